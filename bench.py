@@ -1,0 +1,199 @@
+"""Throughput of the data-parallel hot path on one MI355X.
+
+A step is one full SGD iteration of the 9216-4096-4096-1000 fully connected stack at
+B = 256 (AlexNet-style FC layers, bf16 operands, fp32 accumulation, fp32 master weights,
+ReLU, softmax cross-entropy, update fused into the weight-gradient kernels), on one fixed
+synthetic batch already resident in HBM.
+
+Prints one JSON line: the metric (algorithmic TFLOP/s of fwd + bwd + SGD), samples/s,
+fraction of the bf16 MFMA peak, a roofline entry for the dominant kernel (the layer-1
+weight-gradient kernel with the fused update, timed with HIP events inside the timed
+region's twin) and the CPU oracle timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fwd+bwd+SGD TFLOP/s and samples/s per GPU; % of MFMA dense peak"
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dw_sgd_alexnet_l1_traffic.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_1712_04432_amd", "csrc", f) for f in ("gemm.hip", "common.h")]
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE/WRITE_SIZE
+    runs, kept only while the kernel source is the one the counters were taken on."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def dw_sgd_bytes(d_out: int, d_in: int, batch: int, act_bytes: int = 2) -> int:
+    """Algorithmic bytes of one fused weight-gradient + update launch: the fp32 master is
+    read and written, the bf16 copy written (10 B per parameter), X and Delta_Y read once."""
+    return d_out * d_in * (4 + 4 + 2) + batch * (d_in + d_out) * act_bytes
+
+
+def cpu_baseline(cfg, sample_batch: int = 8):
+    """The oracle, as it is, on one SGD iteration of the same network restricted to
+    `sample_batch` samples (the full weights and update are still processed)."""
+    import numpy as np
+
+    import oracle
+    from synthdata import bf16_bits_to_f32, make_mlp_inputs
+    d = make_mlp_inputs(cfg, seed=0, batch=sample_batch)
+    xv = bf16_bits_to_f32(d["x_bits"]).astype(np.float64)
+    t0 = time.perf_counter()
+    oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, "bf16")
+    dt = time.perf_counter() - t0
+    flops = cfg.gemm_flops(batch=sample_batch)
+    return {"value": round(flops / dt / 1e12, 9), "unit": "TFLOP/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"one SGD iteration of the {'-'.join(map(str, cfg.dims))} stack on {sample_batch} of "
+                      f"the {cfg.batch} samples (full weights and update), bf16-mirrored fp64 oracle, "
+                      f"{dt:.2f} s = {sample_batch / dt:.3f} samples/s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="alexnet_fc_b256")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-batch", type=int, default=8)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
+              f"1.5D grid is not part of it", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_1712_04432_amd as m
+    from synthdata import get_config, make_mlp_inputs
+
+    m.load()
+    cfg = get_config(args.workload)
+    dev = torch.device("cuda:0")
+    log(f"bench: workload {cfg.name} dims {cfg.dims} B={cfg.batch} dtype={cfg.dtype}")
+    d = make_mlp_inputs(cfg, seed=0)
+    net = m.MLP(cfg.dims, cfg.batch, cfg.dtype)
+    layers = []
+    for w, b in zip(d["w"], d["b"]):
+        w32 = torch.from_numpy(w).to(dev)
+        wlp = torch.empty(w.shape, dtype=torch.bfloat16, device=dev)
+        m.cast_f32_bf16(w32, wlp)
+        layers.append({"w": w32, "w_lp": wlp, "b": torch.from_numpy(b).to(dev)})
+    x = torch.from_numpy(d["x_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+    lab = torch.from_numpy(d["labels"]).to(dev)
+    ws = torch.zeros(m.mlp_workspace_bytes(net), dtype=torch.uint8, device=dev)
+    loss = torch.zeros(1, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        m.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    loss0 = loss.item()
+    log(f"bench: warmup done, loss {loss0:.5f}")
+
+    # timed region: K steps between two synchronisations
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / args.steps
+    log(f"bench: {args.steps} steps in {ms_total:.3f} ms (wall {wall * 1e3:.3f} ms), loss {loss.item():.5f}")
+
+    # the same K steps again with HIP events around the dominant kernel (layer-1 fused dW+SGD)
+    m.timing_begin(m.IMBD_K_GEMM_DW, 1, args.steps)
+    for _ in range(args.steps):
+        step()
+    n_launch, k_ms = m.timing_end()
+    torch.cuda.synchronize()
+    k_avg_ms = k_ms / max(n_launch, 1)
+    flops = cfg.gemm_flops()
+    tflops = flops / (ms_step * 1e-3) / 1e12
+    dom_bytes = dw_sgd_bytes(cfg.dims[1], cfg.dims[0], cfg.batch)
+    achieved = dom_bytes / (k_avg_ms * 1e-3) / 1e9
+    traffic = measured_traffic()
+    result = {
+        "metric": METRIC,
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) inputs clamped at 0, uniform labels, He-initialised weights)",
+        "config": {"workload": f"{cfg.name}: {'-'.join(map(str, cfg.dims))} FC stack, ReLU, softmax "
+                               f"cross-entropy, bf16 operands / fp32 accumulation / fp32 masters, fused SGD",
+                   "global_batch": cfg.batch, "layers": cfg.n_layers, "parallelism": "single GPU (P_r = P_c = 1)"},
+        "samples_per_s": round(cfg.batch / (ms_step * 1e-3), 1),
+        "pct_bf16_mfma_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 3),
+        "gflop_per_step": round(flops / 1e9, 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "traffic": traffic,
+                     "kernel": "layer-1 weight gradient with fused SGD (4096x9216 update, K=256)",
+                     "algorithmic_bytes_per_launch": dom_bytes, "avg_launch_ms": round(k_avg_ms, 5),
+                     "launches_timed": n_launch},
+        "loss_first": round(loss0, 6),
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(cfg, args.cpu_sample_batch)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

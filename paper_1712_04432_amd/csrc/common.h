@@ -1,0 +1,116 @@
+// Internal declarations of the gfx950 library behind include/imbd.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "imbd.h"
+
+namespace imbd {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// ------------------------------------------------------------------------- bf16 bits
+// fp32 -> bf16, round to nearest, ties to even; NaN stays a (quiet) NaN. Adding
+// 0x7fff plus the lowest kept bit and truncating rounds the 16 dropped bits to
+// nearest-even, and a carry out of the significand correctly bumps the exponent
+// (largest values overflow to infinity).
+__host__ __device__ inline uint16_t f32_to_bf16(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__host__ __device__ inline float bf16_to_f32(uint16_t h) {
+  return __builtin_bit_cast(float, (uint32_t)h << 16);
+}
+
+// -------------------------------------------------------------------- GEMM epilogue
+// Applied to each accumulated value acc(m, n) of a product; element (m, n) of every
+// output lives at ptr + n*ld + m (m is the contiguous index).
+enum EpiMode { EPI_STORE = 0, EPI_SGD = 1 };
+
+struct Epilogue {
+  int mode = EPI_STORE;
+  float alpha = 1.0f;            // acc scale
+  const float *bias = nullptr;   // STORE: + bias[m] after the scale
+  int relu = 0;                  // STORE: max(., 0) after the bias
+  const void *mask = nullptr;    // STORE: zero where !(mask(m, n) > 0)
+  int64_t ldmask = 0;
+  int mask_dtype = IMBD_BF16;
+  void *out = nullptr;           // STORE: output; SGD: fp32 master weights (read-modify-write)
+  int64_t ldo = 0;
+  int out_dtype = IMBD_F32;
+  uint16_t *out2 = nullptr;      // SGD: bf16 copy of the updated weights (may be null)
+  int64_t ldo2 = 0;
+  float lr = 0.0f;               // SGD: w <- w - lr * alpha * acc
+};
+
+// One product D(m, n) = sum_k A(m, k) B(k, n) for m < M, n < N, k < K.
+//  A(m, k) is at A + m*lda + k when a_kc (k contiguous), else at A + k*lda + m.
+//  B(k, n) is at B + n*ldb + k when b_kc, else at B + k*ldb + n.
+// The three layer products map onto it as (memory is sample-major, W row-major):
+//  forward  Y[b][o]  = sum_i W[o][i] X[b][i]   : m=o, n=b, k=i  (A=W k-contig, B=X k-contig)
+//  dX       dX[b][i] = sum_o W[o][i] dY[b][o]  : m=i, n=b, k=o  (A=W strided,  B=dY k-contig)
+//  dW       dW[o][i] = sum_b X[b][i] dY[b][o]  : m=i, n=o, k=b  (A=X strided,  B=dY strided)
+struct GemmProblem {
+  int dtype = IMBD_BF16;  // operand type, accumulation in fp32
+  const void *A = nullptr;
+  int64_t lda = 0;
+  bool a_kc = true;
+  const void *B = nullptr;
+  int64_t ldb = 0;
+  bool b_kc = true;
+  int M = 0, N = 0, K = 0;
+  Epilogue epi;
+  int kclass = IMBD_K_GEMM_FWD;  // timing tag
+  int layer = 0;
+};
+
+// Launch plan chosen for a product (a pure function of the shapes).
+struct GemmPlan {
+  int cfg;       // tile configuration index
+  int bm, bn;    // tile sizes
+  int splits;    // K splits (1 = no partial sums)
+  int k_split;   // K elements per split (multiple of the K tile)
+  size_t ws_bytes;
+};
+
+GemmPlan gemm_plan(const GemmProblem &p);
+// Enqueue the product; ws must hold plan.ws_bytes (partial sums) when splits > 1.
+int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s);
+
+// ----------------------------------------------------------------- other kernels
+int run_softmax_xent(int B, int C, const float *logits, int64_t ldz, const int32_t *labels,
+                     float inv_batch, float *loss, float *row_loss, void *dz, int64_t lddz,
+                     int dz_dtype, hipStream_t s, int layer);
+int run_bias_grad(int dtype, int M, int B, const void *dy, int64_t lddy, float alpha,
+                  float *db_out, float *bias_sgd, float lr, hipStream_t s, int layer);
+int run_sgd(float *w, uint16_t *w16, const float *g, int64_t n, float step, hipStream_t s,
+            int layer);
+int run_cast(const float *src, uint16_t *dst, int64_t n, hipStream_t s);
+int run_conv_fwd(int N, int H, int W, int Ci, int Co, const void *xp, const void *w, void *y,
+                 int y_dtype, hipStream_t s);
+int run_conv_dgrad(int N, int H, int W, int Ci, int Co, const void *dyp, const void *w, void *dx,
+                   int dx_dtype, hipStream_t s);
+int run_conv_wgrad(int N, int H, int W, int Ci, int Co, const void *xp, const void *dyp,
+                   float *dw, void *ws, size_t ws_bytes, hipStream_t s);
+size_t conv_wgrad_ws_bytes(int N, int H, int W, int Ci, int Co);
+
+// --------------------------------------------------------------------- host helpers
+void set_error(const char *fmt, ...);
+int check_launch(const char *what);
+
+// Records HIP events around one launch when timing is active for (cls, layer).
+struct LaunchTimer {
+  LaunchTimer(int cls, int layer, hipStream_t s);
+  ~LaunchTimer();
+  hipStream_t stream;
+  int slot;
+};
+
+}  // namespace imbd

@@ -1,0 +1,223 @@
+"""Per-kernel parity of the HIP path against the oracle, through the C ABI.
+
+Shapes span several tiles and ragged tails (M, N, K not multiples of the 64/128 tiles,
+K not a multiple of the 8-element vector, single rows/columns)."""
+import numpy as np
+import pytest
+
+import oracle
+from synthdata import make_local_inputs, to_bf16_bits
+from tests._util import TOL_BF16, TOL_F32, bf16_values, dev_bf16_bits, dev_f32, host, nrm_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _flush(msg):
+    print(msg, flush=True)
+
+
+# ------------------------------------------------------------------------------ cast
+def test_cast_f32_bf16_bit_exact(imbd, dev):
+    import torch
+    rng = np.random.default_rng(0)
+    f = np.concatenate([
+        (rng.standard_normal(100003) * 10.0 ** rng.integers(-38, 38, 100003)).astype(np.float32),
+        (np.arange(1, 5000, dtype=np.uint32) << 16 | np.uint32(0x8000)).view(np.float32),   # ties
+        np.array([0.0, -0.0, 1e-45, -1e-45, 3.39e38, 3.4e38, -3.4e38, np.inf, -np.inf], np.float32),
+    ]).astype(np.float32)
+    src = dev_f32(f, dev)
+    dst = torch.empty(f.size, dtype=torch.bfloat16, device=dev)
+    imbd.cast_f32_bf16(src, dst)
+    got = dst.view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = oracle.bf16_bits_of(oracle.round_bf16(f.astype(np.float64)))
+    assert np.array_equal(got, ref)
+    # NaN stays NaN
+    nan = dev_f32(np.array([np.nan], np.float32), dev)
+    out = torch.empty(1, dtype=torch.bfloat16, device=dev)
+    imbd.cast_f32_bf16(nan, out)
+    assert torch.isnan(out.float()).item()
+
+
+# ------------------------------------------------------------------------------- SGD
+@pytest.mark.parametrize("n", [1, 3, 4, 1000, 1 << 20, (1 << 20) + 7])
+def test_sgd_step_bit_exact(imbd, dev, n):
+    """Eq. (1): w - lr*g with one fp32 rounding; lr given as the fp32 value both sides use."""
+    import torch
+    rng = np.random.default_rng(n)
+    w = rng.standard_normal(n).astype(np.float32)
+    g = rng.standard_normal(n).astype(np.float32)
+    lr = float(np.float32(0.01))
+    wd, gd = dev_f32(w, dev), dev_f32(g, dev)
+    w16 = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    imbd.sgd_step(wd, gd, lr, 1.0, w_lp=w16)
+    ref = oracle.round_to(oracle.sgd(w, g, lr), "f32")
+    assert np.array_equal(wd.cpu().numpy().astype(np.float64), ref)
+    assert np.array_equal(w16.view(torch.int16).cpu().numpy().view(np.uint16),
+                          oracle.bf16_bits_of(oracle.round_bf16(ref)))
+
+
+def test_sgd_step_unaligned_and_scaled(imbd, dev):
+    rng = np.random.default_rng(5)
+    w = rng.standard_normal(1001).astype(np.float32)
+    g = rng.standard_normal(1001).astype(np.float32)
+    base = dev_f32(np.concatenate([[0], w]), dev)
+    gb = dev_f32(np.concatenate([[0], g]), dev)
+    wd, gd = base[1:], gb[1:]                       # 4-byte offset: scalar kernel
+    imbd.sgd_step(wd, gd, 0.5, 0.25)
+    step = float(np.float32(np.float32(0.5) * np.float32(0.25)))
+    ref = oracle.round_to(oracle.sgd(w, g, step), "f32")
+    assert np.array_equal(wd.cpu().numpy().astype(np.float64), ref)
+
+
+# --------------------------------------------------------------------------- softmax
+@pytest.mark.parametrize("B,C,dz_dtype", [(64, 10, "f32"), (256, 1000, "bf16"), (256, 1000, "f32"),
+                                          (5, 3, "f32"), (1, 1, "f32"), (33, 129, "bf16")])
+def test_softmax_xent(imbd, dev, B, C, dz_dtype):
+    import torch
+    rng = np.random.default_rng(B * 1000 + C)
+    z = (rng.standard_normal((B, C)) * 4).astype(np.float32)
+    lab = rng.integers(0, C, B).astype(np.int32)
+    zd = dev_f32(z, dev)
+    ld = torch.from_numpy(lab).to(dev)
+    loss = torch.zeros(1, device=dev)
+    rows = torch.zeros(B, device=dev)
+    dz = torch.empty((B, C), device=dev, dtype=torch.bfloat16 if dz_dtype == "bf16" else torch.float32)
+    imbd.softmax_xent(zd, ld, 1.0 / B, loss, rows, dz)
+    rl, rdz, rrows = oracle.softmax_xent(z, lab, 1.0 / B)
+    assert abs(loss.item() - rl) <= 1e-5 * max(1.0, abs(rl))
+    assert nrm_err(host(rows), rrows) < 1e-5
+    tol = TOL_BF16 if dz_dtype == "bf16" else TOL_F32
+    assert nrm_err(host(dz), rdz) < tol
+    if dz_dtype == "bf16":
+        assert nrm_err(host(dz), rdz) < 2.0 ** -8
+    else:
+        assert nrm_err(host(dz), rdz) < 1e-6
+
+
+def test_softmax_bad_label_gives_nan_not_a_fault(imbd, dev):
+    import torch
+    z = dev_f32(np.zeros((4, 10), np.float32), dev)
+    lab = torch.tensor([0, 10, -1, 9], dtype=torch.int32, device=dev)
+    loss = torch.zeros(1, device=dev)
+    rows = torch.zeros(4, device=dev)
+    imbd.softmax_xent(z, lab, 0.25, loss, rows)
+    r = rows.cpu().numpy()
+    assert np.isnan(r[1]) and np.isnan(r[2])
+    assert r[0] == pytest.approx(np.log(10), rel=1e-6) and r[3] == pytest.approx(np.log(10), rel=1e-6)
+
+
+# ------------------------------------------------------------------ local products
+LOCAL_SHAPES = [
+    # d_out_blk, d_in, b_blk
+    (256, 784, 64), (128, 256, 64), (10, 128, 64),             # the 784-256-128-10 layers
+    (1024, 4096, 64), (250, 4096, 64),                          # 4 x 16 grid blocks
+    (130, 200, 70), (37, 100, 13), (1, 1, 1), (64, 64, 64), (129, 65, 257), (3, 8, 5),
+    (200, 1000, 128),
+]
+
+
+def _local_inputs(dout, din, b, dtype, seed=0):
+    d = make_local_inputs(dout, din, b, seed=seed, dtype=dtype)
+    if dtype == "bf16":
+        return d, bf16_values(d["w_bits"]), bf16_values(d["x_bits"]), bf16_values(d["dy_bits"])
+    return d, d["w"].astype(np.float64), d["x"].astype(np.float64), d["dy"].astype(np.float64)
+
+
+def _to_dev(d, key, dtype, dev):
+    return dev_bf16_bits(d[key + "_bits"], dev) if dtype == "bf16" else dev_f32(d[key], dev)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", LOCAL_SHAPES)
+def test_local_fwd_parity(imbd, dev, dtype, shape):
+    import torch
+    dout, din, b = shape
+    _flush(f"local_fwd {dtype} {shape}")
+    d, W, X, _ = _local_inputs(dout, din, b, dtype)
+    wd, xd = _to_dev(d, "w", dtype, dev), _to_dev(d, "x", dtype, dev)
+    bias = dev_f32(d["b"], dev)
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(0, imbd.dtype_code(wd), dout, din, b), 16),
+                     dtype=torch.uint8, device=dev)
+    ref = oracle.local_fwd(W, X, d["b"].astype(np.float64), apply_relu=False)
+    y32 = torch.empty((b, dout), device=dev)
+    imbd.mlp_local_fwd(wd, xd, y32, 4, 16, bias=bias, relu=False, ws=ws)
+    assert nrm_err(host(y32), ref) < 1e-5          # only fp32 accumulation differs
+    yr = torch.empty((b, dout), device=dev, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32)
+    imbd.mlp_local_fwd(wd, xd, yr, 4, 16, bias=bias, relu=True, ws=ws)
+    rr = oracle.relu(ref)
+    tol = TOL_BF16 if dtype == "bf16" else TOL_F32
+    assert nrm_err(host(yr), oracle.round_to(rr, dtype)) < tol
+    if dtype == "bf16":
+        assert nrm_err(host(yr), rr) < 2.0 ** -8
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", LOCAL_SHAPES)
+def test_local_bwd_parity(imbd, dev, dtype, shape):
+    import torch
+    dout, din, b = shape
+    _flush(f"local_bwd {dtype} {shape}")
+    P_r, P_c = 4, 16
+    d, W, X, DY = _local_inputs(dout, din, b, dtype, seed=1)
+    wd, xd, dyd = _to_dev(d, "w", dtype, dev), _to_dev(d, "x", dtype, dev), _to_dev(d, "dy", dtype, dev)
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(1, imbd.dtype_code(wd), dout, din, b), 16),
+                     dtype=torch.uint8, device=dev)
+    dw = torch.empty((dout, din), device=dev)
+    db = torch.empty(dout, device=dev)
+    dx = torch.empty((b, din), device=dev)
+    imbd.mlp_local_bwd(wd, dyd, xd, dw, P_r, P_c, db_part=db, dx_part=dx, mask_relu=True, ws=ws)
+    scale = 1.0 / (b * P_c)
+    rdw, rdb, rdx = oracle.local_bwd(W, DY, X, scale, mask_src=X)
+    assert nrm_err(host(dw), rdw) < 1e-5
+    assert nrm_err(host(db), rdb) < 1e-5
+    assert nrm_err(host(dx), rdx) < 1e-5
+    # unmasked partial
+    imbd.mlp_local_bwd(wd, dyd, xd, dw, P_r, P_c, dx_part=dx, mask_relu=False, ws=ws)
+    assert nrm_err(host(dx), oracle.input_grad(W, DY)) < 1e-5
+
+
+def test_local_fwd_strided_views(imbd, dev):
+    """Blocks passed as views of a larger array (leading dimension > row length)."""
+    import torch
+    rng = np.random.default_rng(3)
+    Wf = rng.standard_normal((300, 520)).astype(np.float32)
+    Xf = rng.standard_normal((96, 520)).astype(np.float32)
+    Wb, Xb = to_bf16_bits(Wf), to_bf16_bits(Xf)
+    wd, xd = dev_bf16_bits(Wb, dev), dev_bf16_bits(Xb, dev)
+    Wv, Xv = bf16_values(Wb), bf16_values(Xb)
+    # process (r, c) = (1, 2) of a 3 x 4 grid over W rows and X rows, columns 8..520
+    wblk, xblk = wd[100:200, 8:520], xd[48:72, 8:520]
+    ybig = torch.zeros((24, 300), device=dev)
+    yblk = ybig[:, 100:200]
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(0, 1, 100, 512, 24), 16), dtype=torch.uint8, device=dev)
+    imbd.mlp_local_fwd(wblk, xblk, yblk, 3, 4, ws=ws)
+    ref = oracle.affine_fwd(Wv[100:200, 8:520], Xv[48:72, 8:520])
+    assert nrm_err(host(yblk), ref) < 1e-5
+    assert torch.count_nonzero(ybig[:, :100]).item() == 0 and torch.count_nonzero(ybig[:, 200:]).item() == 0
+
+
+def test_local_bwd_empty_block_writes_zero_partials(imbd, dev):
+    import torch
+    dw = torch.full((5, 7), 3.0, device=dev)
+    db = torch.full((5,), 3.0, device=dev)
+    w = torch.zeros((5, 7), dtype=torch.bfloat16, device=dev)
+    x = torch.zeros((0, 7), dtype=torch.bfloat16, device=dev)
+    dy = torch.zeros((0, 5), dtype=torch.bfloat16, device=dev)
+    imbd.mlp_local_bwd(w, dy, x, dw, 2, 2, db_part=db)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(dw).item() == 0 and torch.count_nonzero(db).item() == 0
+
+
+def test_split_k_is_deterministic(imbd, dev):
+    """Long-K products split K over workgroups; partial sums are added in a fixed order."""
+    import torch
+    d, W, X, _ = _local_inputs(512, 9216, 64, "bf16", seed=7)
+    wd, xd = _to_dev(d, "w", "bf16", dev), _to_dev(d, "x", "bf16", dev)
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(0, 1, 512, 9216, 64), 16), dtype=torch.uint8, device=dev)
+    assert imbd.mlp_local_workspace_bytes(0, 1, 512, 9216, 64) > 0          # it does split
+    y1 = torch.empty((64, 512), device=dev)
+    y2 = torch.empty((64, 512), device=dev)
+    imbd.mlp_local_fwd(wd, xd, y1, 1, 1, ws=ws)
+    imbd.mlp_local_fwd(wd, xd, y2, 1, 1, ws=ws)
+    assert torch.equal(y1, y2)
+    assert nrm_err(host(y1), oracle.affine_fwd(W, X)) < 1e-5
