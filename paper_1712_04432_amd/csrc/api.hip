@@ -280,7 +280,7 @@ int mlp_bwd(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, void *ws,
   if (fuse_sgd && !std::isfinite(lr)) FAIL(IMBD_EINVAL, "lr must be finite");
   TRY(check_ws(lay, ws, ws_bytes));
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const int L = d->n_layers, B = d->batch;
+  const int L = d->n_layers;
   void *part = at(ws, lay.partial);
   for (int i = L; i >= 1; --i) {
     imbd_layer &ly = layers[i - 1];
@@ -304,11 +304,14 @@ int mlp_bwd(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, void *ws,
       e.out_dtype = d->dtype;
       TRY(gemm_run(p, part, lay.partial_bytes, s));
     }
-    TRY(run_bias_grad(d->dtype, d->dims[i], B, dy, d->dims[i], 1.0f, fuse_sgd ? nullptr : ly.db,
-                      fuse_sgd ? ly.b : nullptr, lr, s, i));
+    // Delta_W_i with the bias gradient from the same pass (row sums of the Delta_Y tile)
     GemmProblem p = dw_problem(d, i);
     p.A = xi;
     p.B = dy;
+    p.db_mode = fuse_sgd ? 2 : 1;
+    p.db_out = ly.db;
+    p.bias = ly.b;
+    p.bias_lr = lr;
     Epilogue &e = p.epi;
     if (fuse_sgd) {
       e.mode = EPI_SGD;
@@ -466,12 +469,16 @@ int mlp_local_bwd(int dtype, int P_r, int P_c, int d_out_blk, int d_in, int b_bl
     p.epi.out_dtype = IMBD_F32;
     TRY(gemm_run(p, ws, ws_bytes, s));
   }
-  if (db_part) TRY(run_bias_grad(dtype, d_out_blk, b_blk, dy_blk, lddy, scale, db_part, nullptr, 0.f, s, 0));
   GemmProblem p = local_dw_problem(dtype, d_out_blk, d_in, b_blk);
   p.A = x_blk;
   p.lda = ldx;
   p.B = dy_blk;
   p.ldb = lddy;
+  if (db_part) {
+    p.db_mode = 1;
+    p.db_out = db_part;
+    p.db_alpha = scale;
+  }
   p.epi.mode = EPI_STORE;
   p.epi.alpha = scale;
   p.epi.out = dw_part;

@@ -67,6 +67,14 @@ struct GemmProblem {
   bool b_kc = true;
   int M = 0, N = 0, K = 0;
   Epilogue epi;
+  // Sums of the B operand over k, db(n) = db_alpha * sum_k B(k, n), for the weight-gradient
+  // product (B = Delta_Y stored [b][n], k = sample): the bias gradient comes out of the
+  // same pass. db_mode 0: none, 1: store db_out[n], 2: bias[n] -= bias_lr * db(n).
+  int db_mode = 0;
+  float *db_out = nullptr;
+  float *bias = nullptr;
+  float db_alpha = 1.0f;
+  float bias_lr = 0.0f;
   int kclass = IMBD_K_GEMM_FWD;  // timing tag
   int layer = 0;
 };

@@ -60,6 +60,8 @@ struct KcLoader {
   static constexpr int PER = (CH + NT - 1) / NT;
   u32x4 v[PER];
 
+  // G: guarded (edge tile: masked, possibly unaligned); !G: interior tile, plain loads
+  template <bool G>
   __device__ __forceinline__ void load(const T *base, int64_t ld, int row0, int rows, int k0,
                                        int kend, bool vec_ok, int tid) {
 #pragma unroll
@@ -69,8 +71,13 @@ struct KcLoader {
         const int r = c >> 3, kc = c & 7;
         const int grow = row0 + r;
         const int kk = k0 + kc * VEC;
-        const int valid = (grow < rows) ? (kend - kk) : 0;
-        v[i] = load16<T>(base + (int64_t)grow * ld + kk, valid, vec_ok);
+        const T *p = base + (int64_t)grow * ld + kk;
+        if constexpr (G) {
+          const int valid = (grow < rows) ? (kend - kk) : 0;
+          v[i] = load16<T>(p, valid, vec_ok);
+        } else {
+          v[i] = *reinterpret_cast<const u32x4 *>(p);
+        }
       }
     }
   }
@@ -97,6 +104,7 @@ struct TrLoader {
   static constexpr int PER = (NB + NT - 1) / NT;
   u32x4 v[PER][VEC];
 
+  template <bool G>
   __device__ __forceinline__ void load(const T *base, int64_t ld, int row0, int rows, int k0,
                                        int kend, bool vec_ok, int tid) {
 #pragma unroll
@@ -108,8 +116,13 @@ struct TrLoader {
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
           const int k = k0 + kb * VEC + j;
-          const int valid = (k < kend) ? (rows - col) : 0;
-          v[i][j] = load16<T>(base + (int64_t)k * ld + col, valid, vec_ok);
+          const T *p = base + (int64_t)k * ld + col;
+          if constexpr (G) {
+            const int valid = (k < kend) ? (rows - col) : 0;
+            v[i][j] = load16<T>(p, valid, vec_ok);
+          } else {
+            v[i][j] = *reinterpret_cast<const u32x4 *>(p);
+          }
         }
       }
     }
@@ -153,80 +166,112 @@ struct LoaderSel<T, R, NT, true> { using type = KcLoader<T, R, NT>; };
 template <typename T, int R, int NT>
 struct LoaderSel<T, R, NT, false> { using type = TrLoader<T, R, NT>; };
 
+template <bool B>
+struct BoolTag {
+  static constexpr bool value = B;
+};
+
 struct KArgs {
   const void *A;
   const void *B;
   int64_t lda, ldb;
   int M, N, K;
   int k_split, splits, tiles_m, tiles_n;
-  int a_vec, b_vec, out_vec;
+  int a_vec, b_vec, out_vec, mask_vec, bias_vec;
   Epilogue epi;
-  float *partial;  // [splits][N][ldp] when splits > 1
-  int64_t ldp;
+  float *partial;  // [splits][sstride] of [N][ldp] rows when splits > 1
+  int64_t ldp, sstride;
+  int db_mode;     // see GemmProblem
+  float *db_out;
+  float *bias;
+  float db_alpha, bias_lr;
 };
 
 // ------------------------------------------------------------------------- epilogue
-__device__ __forceinline__ bool mask_keep(const Epilogue &e, int m, int n) {
-  if (!e.mask) return true;
+__device__ __forceinline__ float mask_at(const Epilogue &e, int m, int n) {
   const int64_t off = (int64_t)n * e.ldmask + m;
-  const float v = (e.mask_dtype == IMBD_BF16)
-                      ? bf16_to_f32(reinterpret_cast<const uint16_t *>(e.mask)[off])
-                      : reinterpret_cast<const float *>(e.mask)[off];
-  return v > 0.0f;
+  return (e.mask_dtype == IMBD_BF16) ? bf16_to_f32(reinterpret_cast<const uint16_t *>(e.mask)[off])
+                                     : reinterpret_cast<const float *>(e.mask)[off];
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
 }
 
 // Finish up to 4 consecutive outputs (m..m+3, n); v holds the accumulated sums.
-__device__ __forceinline__ void epilogue4(const Epilogue &e, int M, int m, int n, const float v[4],
-                                          bool vec_ok) {
-  const int cnt = (M - m) < 4 ? (M - m) : 4;
+__device__ __forceinline__ void epilogue4(const KArgs &g, int m, int n, const float v[4]) {
+  const Epilogue &e = g.epi;
+  const int cnt = (g.M - m) < 4 ? (g.M - m) : 4;
+  const bool vec = cnt == 4 && g.out_vec;
   if (e.mode == EPI_SGD) {
     float *w = reinterpret_cast<float *>(e.out) + (int64_t)n * e.ldo + m;
-    float nw[4];
-    if (cnt == 4 && vec_ok) {
-      f32x4 old = *reinterpret_cast<const f32x4 *>(w);
+    if (vec) {
+      const f32x4 old = *reinterpret_cast<const f32x4 *>(w);
+      f32x4 nw;
 #pragma unroll
       for (int i = 0; i < 4; ++i) nw[i] = fmaf(-e.lr, e.alpha * v[i], old[i]);
-      *reinterpret_cast<f32x4 *>(w) = f32x4{nw[0], nw[1], nw[2], nw[3]};
+      *reinterpret_cast<f32x4 *>(w) = nw;
       if (e.out2) {
-        uint16_t *w2 = e.out2 + (int64_t)n * e.ldo2 + m;
         u32x2 pk;
-        pk[0] = (uint32_t)f32_to_bf16(nw[0]) | ((uint32_t)f32_to_bf16(nw[1]) << 16);
-        pk[1] = (uint32_t)f32_to_bf16(nw[2]) | ((uint32_t)f32_to_bf16(nw[3]) << 16);
-        *reinterpret_cast<u32x2 *>(w2) = pk;
+        pk[0] = pack_bf16x2(nw[0], nw[1]);
+        pk[1] = pack_bf16x2(nw[2], nw[3]);
+        *reinterpret_cast<u32x2 *>(e.out2 + (int64_t)n * e.ldo2 + m) = pk;
       }
     } else {
       for (int i = 0; i < cnt; ++i) {
-        nw[i] = fmaf(-e.lr, e.alpha * v[i], w[i]);
-        w[i] = nw[i];
-        if (e.out2) e.out2[(int64_t)n * e.ldo2 + m + i] = f32_to_bf16(nw[i]);
+        const float nw = fmaf(-e.lr, e.alpha * v[i], w[i]);
+        w[i] = nw;
+        if (e.out2) e.out2[(int64_t)n * e.ldo2 + m + i] = f32_to_bf16(nw);
       }
     }
     return;
   }
-  float x[4];
+  float x[4], bias[4] = {0.f, 0.f, 0.f, 0.f}, keep[4] = {1.f, 1.f, 1.f, 1.f};
+  if (e.bias) {
+    if (cnt == 4 && g.bias_vec) {
+      const f32x4 b4 = *reinterpret_cast<const f32x4 *>(e.bias + m);
+      bias[0] = b4[0]; bias[1] = b4[1]; bias[2] = b4[2]; bias[3] = b4[3];
+    } else {
+      for (int i = 0; i < cnt; ++i) bias[i] = e.bias[m + i];
+    }
+  }
+  if (e.mask) {
+    if (cnt == 4 && g.mask_vec) {
+      const int64_t off = (int64_t)n * e.ldmask + m;
+      if (e.mask_dtype == IMBD_BF16) {
+        const u32x2 mk = *reinterpret_cast<const u32x2 *>(reinterpret_cast<const uint16_t *>(e.mask) + off);
+        keep[0] = bf16_to_f32((uint16_t)(mk[0] & 0xffffu)) > 0.f;
+        keep[1] = bf16_to_f32((uint16_t)(mk[0] >> 16)) > 0.f;
+        keep[2] = bf16_to_f32((uint16_t)(mk[1] & 0xffffu)) > 0.f;
+        keep[3] = bf16_to_f32((uint16_t)(mk[1] >> 16)) > 0.f;
+      } else {
+        const f32x4 mk = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(e.mask) + off);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) keep[i] = mk[i] > 0.f;
+      }
+    } else {
+      for (int i = 0; i < cnt; ++i) keep[i] = mask_at(e, m + i, n) > 0.f;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    float t = e.alpha * v[i];
-    if (i < cnt) {
-      if (e.bias) t += e.bias[m + i];
-      if (e.relu) t = t > 0.0f ? t : 0.0f;
-      if (!mask_keep(e, m + i, n)) t = 0.0f;
-    }
-    x[i] = t;
+    float t = e.alpha * v[i] + bias[i];
+    if (e.relu) t = t > 0.0f ? t : 0.0f;
+    x[i] = keep[i] != 0.f ? t : 0.0f;
   }
   if (e.out_dtype == IMBD_BF16) {
     uint16_t *o = reinterpret_cast<uint16_t *>(e.out) + (int64_t)n * e.ldo + m;
-    if (cnt == 4 && vec_ok) {
+    if (vec) {
       u32x2 pk;
-      pk[0] = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-      pk[1] = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
+      pk[0] = pack_bf16x2(x[0], x[1]);
+      pk[1] = pack_bf16x2(x[2], x[3]);
       *reinterpret_cast<u32x2 *>(o) = pk;
     } else {
       for (int i = 0; i < cnt; ++i) o[i] = f32_to_bf16(x[i]);
     }
   } else {
     float *o = reinterpret_cast<float *>(e.out) + (int64_t)n * e.ldo + m;
-    if (cnt == 4 && vec_ok) {
+    if (vec) {
       *reinterpret_cast<f32x4 *>(o) = f32x4{x[0], x[1], x[2], x[3]};
     } else {
       for (int i = 0; i < cnt; ++i) o[i] = x[i];
@@ -236,17 +281,32 @@ __device__ __forceinline__ void epilogue4(const Epilogue &e, int M, int m, int n
 
 // --------------------------------------------------------------------------- kernel
 template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, bool A_KC, bool B_KC>
-__global__ void __launch_bounds__(64 * WAVES_M *WAVES_N)
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
     gemm_kernel(KArgs g) {
   constexpr int NT = 64 * WAVES_M * WAVES_N;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int FM = WM / 16, FN = WN / 16;
+  constexpr int VEC = Elem<T>::VEC;
   constexpr int BK = KT_BYTES / (int)sizeof(T);
   constexpr int STAGE_A = BM * LDS_PITCH, STAGE = (BM + BN) * LDS_PITCH;
+  // Transposed loaders use a fraction of the threads; when both fit in half the block,
+  // the B loader runs on the other half.
+  constexpr int NB_A = A_KC ? BM * 8 : 8 * (BM / VEC);
+  constexpr int NB_B = B_KC ? BN * 8 : 8 * (BN / VEC);
+  constexpr int XOR_B = (NB_A <= NT / 2 && NB_B <= NT / 2) ? NT / 2 : 0;
+  // The weight-gradient product (both operands strided) is the one that carries the
+  // fused update; its old master tile is fetched before the K loop so the read half of
+  // the read-modify-write overlaps the products.
+  constexpr bool PREFETCH_W = !A_KC && !B_KC;
+  // Row sums of the B tile (the bias gradient), NT/BN threads per row.
+  constexpr int TPR = NT / BN;
+  constexpr int CPT = 8 / TPR;  // 16-byte chunks per thread per K tile
   static_assert(WM % 16 == 0 && WN % 16 == 0, "wave tile must be a multiple of 16");
+  static_assert(NT % BN == 0 && (TPR == 1 || TPR == 2 || TPR == 4 || TPR == 8), "row-sum split");
   __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x;
+  const int tid_b = tid ^ XOR_B;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave % WAVES_M) * WM, wn0 = (wave / WAVES_M) * WN;
 
@@ -258,17 +318,47 @@ __global__ void __launch_bounds__(64 * WAVES_M *WAVES_N)
   const int per_split = g.tiles_m * g.tiles_n;
   const int s = bid / per_split;
   const int rem = bid - s * per_split;
-  const int tn = rem / g.tiles_m;
-  const int tm = rem - tn * g.tiles_m;
+  // n fastest: the tiles that share an A tile (a W row block, or an X column block in
+  // the weight gradient) run back to back on one XCD and share its L2
+  const int tm = rem / g.tiles_n;
+  const int tn = rem - tm * g.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
   const int kbeg = s * g.k_split;
   const int kend = min(g.K, kbeg + g.k_split);
   const int nk = (kend > kbeg) ? (kend - kbeg + BK - 1) / BK : 0;
+  const int fr = lane & 15, fg = lane >> 4;
+
+  // Full tiles finish through LDS (see the end of the kernel): 32 threads cover one row of
+  // BM outputs, so every store instruction writes whole contiguous rows.
+  constexpr int TPRW = BM / 4;            // threads per output row (4 outputs each)
+  constexpr int RPP = NT / TPRW;          // rows per pass
+  constexpr int PASSES = BN / RPP;
+  static_assert(NT % TPRW == 0 && BN % RPP == 0, "staged epilogue shape");
+  const int er = tid / TPRW, ec = (tid % TPRW) * 4;
+  const bool full_tile = (m0 + BM <= g.M) && (n0 + BN <= g.N) && g.out_vec;
+  const bool sgd_fast = PREFETCH_W && full_tile && g.splits == 1 && g.epi.mode == EPI_SGD;
+  f32x4 wold[PREFETCH_W ? PASSES : 1];
+  if constexpr (PREFETCH_W) {
+    if (sgd_fast) {
+      const float *w = reinterpret_cast<const float *>(g.epi.out);
+#pragma unroll
+      for (int p = 0; p < PASSES; ++p) {
+        const int n = n0 + p * RPP + er;
+        wold[p] = *reinterpret_cast<const f32x4 *>(w + (int64_t)n * g.epi.ldo + m0 + ec);
+      }
+    }
+  }
+  const bool do_db = g.db_mode != 0 && tm == 0 && g.splits == 1;
+  float dbsum = 0.f;
 
   const T *A = reinterpret_cast<const T *>(g.A);
   const T *Bp = reinterpret_cast<const T *>(g.B);
-  typename LoaderSel<T, BM, NT, A_KC>::type la;
-  typename LoaderSel<T, BN, NT, B_KC>::type lb;
+  // Two register stages: while tile kt is multiplied out of LDS, the global loads of
+  // tiles kt+1 and kt+2 are both in flight. The weight-gradient product (short K, its
+  // registers taken by the prefetched master tile) keeps one stage.
+  constexpr int NSTAGE = PREFETCH_W ? 1 : 2;
+  typename LoaderSel<T, BM, NT, A_KC>::type la[NSTAGE];
+  typename LoaderSel<T, BN, NT, B_KC>::type lb[NSTAGE];
 
   f32x4 acc[FM][FN];
 #pragma unroll
@@ -276,22 +366,14 @@ __global__ void __launch_bounds__(64 * WAVES_M *WAVES_N)
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (nk > 0) {
-    la.load(A, g.lda, m0, g.M, kbeg, kend, g.a_vec, tid);
-    lb.load(Bp, g.ldb, n0, g.N, kbeg, kend, g.b_vec, tid);
-    la.store(smem, tid);
-    lb.store(smem + STAGE_A, tid);
-  }
-  __syncthreads();
+  // Interior tiles (every row, column and K tile in range, 16-byte aligned operands) run
+  // the main loop with plain vector loads and no branches around them, so the compiler's
+  // wait counts cover exactly the tile being stored (the last iterations re-load the last
+  // tile instead of skipping the load). Edge tiles run it with masked, conditional loads.
+  const bool interior = (m0 + BM <= g.M) && (n0 + BN <= g.N) && ((kend - kbeg) % BK == 0) &&
+                        g.a_vec && g.b_vec && nk > 0 && (nk % NSTAGE == 0);
 
-  const int fr = lane & 15, fg = lane >> 4;
-  for (int kt = 0; kt < nk; ++kt) {
-    const bool more = (kt + 1) < nk;
-    if (more) {
-      const int k0 = kbeg + (kt + 1) * BK;
-      la.load(A, g.lda, m0, g.M, k0, kend, g.a_vec, tid);
-      lb.load(Bp, g.ldb, n0, g.N, k0, kend, g.b_vec, tid);
-    }
+  auto compute = [&](int kt) {
     const char *sa = smem + (kt & 1) * STAGE;
     const char *sb = sa + STAGE_A;
 #pragma unroll
@@ -322,12 +404,145 @@ __global__ void __launch_bounds__(64 * WAVES_M *WAVES_N)
           }
         }
     }
-    if (more) {
-      char *dst = smem + ((kt + 1) & 1) * STAGE;
-      la.store(dst, tid);
-      lb.store(dst + STAGE_A, tid);
+    if (do_db) {
+      // this thread's share of row tid/TPR of the B tile, in k order
+      const char *row = sb + (tid / TPR) * LDS_PITCH + (tid % TPR) * CPT * 16;
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) {
+        const u32x4 q = *reinterpret_cast<const u32x4 *>(row + c * 16);
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            dbsum += bf16_to_f32((uint16_t)(q[w] & 0xffffu));
+            dbsum += bf16_to_f32((uint16_t)(q[w] >> 16));
+          }
+        } else {
+          const f32x4 qf = __builtin_bit_cast(f32x4, q);  // whole-vector cast (see above)
+          dbsum += qf.x;
+          dbsum += qf.y;
+          dbsum += qf.z;
+          dbsum += qf.w;
+        }
+      }
+    }
+  };
+  auto buf = [&](int kt) { return smem + (kt & 1) * STAGE; };
+
+  if (interior) {
+    auto ktile = [&](int kt) { return kbeg + min(kt, nk - 1) * BK; };
+    la[0].template load<false>(A, g.lda, m0, g.M, ktile(0), kend, true, tid);
+    lb[0].template load<false>(Bp, g.ldb, n0, g.N, ktile(0), kend, true, tid_b);
+    la[0].store(buf(0), tid);
+    lb[0].store(buf(0) + STAGE_A, tid_b);
+    if constexpr (NSTAGE == 2) {
+      la[1].template load<false>(A, g.lda, m0, g.M, ktile(1), kend, true, tid);
+      lb[1].template load<false>(Bp, g.ldb, n0, g.N, ktile(1), kend, true, tid_b);
     }
     __syncthreads();
+    for (int kt = 0; kt < nk; kt += NSTAGE) {
+      if constexpr (NSTAGE == 2) {
+        // step kt: set 1 holds tile kt+1; set 0 receives tile kt+2
+        la[0].template load<false>(A, g.lda, m0, g.M, ktile(kt + 2), kend, true, tid);
+        lb[0].template load<false>(Bp, g.ldb, n0, g.N, ktile(kt + 2), kend, true, tid_b);
+        compute(kt);
+        la[1].store(buf(kt + 1), tid);
+        lb[1].store(buf(kt + 1) + STAGE_A, tid_b);
+        __syncthreads();
+        // step kt+1: set 0 holds tile kt+2; set 1 receives tile kt+3
+        la[1].template load<false>(A, g.lda, m0, g.M, ktile(kt + 3), kend, true, tid);
+        lb[1].template load<false>(Bp, g.ldb, n0, g.N, ktile(kt + 3), kend, true, tid_b);
+        compute(kt + 1);
+        la[0].store(buf(kt + 2), tid);
+        lb[0].store(buf(kt + 2) + STAGE_A, tid_b);
+        __syncthreads();
+      } else {
+        la[0].template load<false>(A, g.lda, m0, g.M, ktile(kt + 1), kend, true, tid);
+        lb[0].template load<false>(Bp, g.ldb, n0, g.N, ktile(kt + 1), kend, true, tid_b);
+        compute(kt);
+        la[0].store(buf(kt + 1), tid);
+        lb[0].store(buf(kt + 1) + STAGE_A, tid_b);
+        __syncthreads();
+      }
+    }
+  } else {
+    // edge tiles: masked loads, one register stage
+    if (nk > 0) {
+      la[0].template load<true>(A, g.lda, m0, g.M, kbeg, kend, g.a_vec, tid);
+      lb[0].template load<true>(Bp, g.ldb, n0, g.N, kbeg, kend, g.b_vec, tid_b);
+      la[0].store(buf(0), tid);
+      lb[0].store(buf(0) + STAGE_A, tid_b);
+    }
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const bool more = kt + 1 < nk;
+      if (more) {
+        la[0].template load<true>(A, g.lda, m0, g.M, kbeg + (kt + 1) * BK, kend, g.a_vec, tid);
+        lb[0].template load<true>(Bp, g.ldb, n0, g.N, kbeg + (kt + 1) * BK, kend, g.b_vec, tid_b);
+      }
+      compute(kt);
+      if (more) {
+        la[0].store(buf(kt + 1), tid);
+        lb[0].store(buf(kt + 1) + STAGE_A, tid_b);
+      }
+      __syncthreads();
+    }
+  }
+
+  if (do_db) {
+    // combine the TPR consecutive threads of a row (commutative pairwise adds: every
+    // lane of the group gets the same bits)
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) dbsum += __shfl_xor(dbsum, o, 64);
+    const int n = n0 + tid / TPR;
+    if (tid % TPR == 0 && n < g.N) {
+      const float gb = g.db_alpha * dbsum;
+      if (g.db_mode == 1) g.db_out[n] = gb;
+      else g.bias[n] = fmaf(-g.bias_lr, gb, g.bias[n]);
+    }
+  }
+
+  if (full_tile) {
+    // Stage the accumulator tile in LDS as [n][m] (pitch BM+4 floats), then let each group
+    // of TPRW threads finish one whole row per pass.
+    constexpr int PT = BM + 4;
+    static_assert(BN * PT * 4 <= 2 * STAGE, "staged tile must fit the operand buffers");
+    float *stg = reinterpret_cast<float *>(smem);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        *reinterpret_cast<f32x4 *>(stg + (wn0 + j * 16 + fr) * PT + wm0 + i * 16 + fg * 4) = acc[i][j];
+    __syncthreads();
+    const int m = m0 + ec;
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int nl = p * RPP + er;
+      const int n = n0 + nl;
+      const f32x4 a = *reinterpret_cast<const f32x4 *>(stg + nl * PT + ec);
+      if (g.splits > 1) {
+        *reinterpret_cast<f32x4 *>(g.partial + (int64_t)s * g.sstride + (int64_t)n * g.ldp + m) = a;
+        continue;
+      }
+      if constexpr (PREFETCH_W) {
+        if (sgd_fast) {
+          const Epilogue &e = g.epi;
+          f32x4 nw;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) nw[q] = fmaf(-e.lr, e.alpha * a[q], wold[p][q]);
+          *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(e.out) + (int64_t)n * e.ldo + m) = nw;
+          if (e.out2) {
+            u32x2 pk;
+            pk[0] = pack_bf16x2(nw[0], nw[1]);
+            pk[1] = pack_bf16x2(nw[2], nw[3]);
+            *reinterpret_cast<u32x2 *>(e.out2 + (int64_t)n * e.ldo2 + m) = pk;
+          }
+          continue;
+        }
+      }
+      const float v[4] = {a[0], a[1], a[2], a[3]};
+      epilogue4(g, m, n, v);
+    }
+    return;
   }
 
   // Accumulator layout of a 16x16 block: lane holds rows 4*(lane/16)..+3 of column lane%16.
@@ -340,9 +555,9 @@ __global__ void __launch_bounds__(64 * WAVES_M *WAVES_N)
       if (m >= g.M || n >= g.N) continue;
       const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
       if (g.splits == 1) {
-        epilogue4(g.epi, g.M, m, n, v, g.out_vec);
+        epilogue4(g, m, n, v);
       } else {
-        float *p = g.partial + ((int64_t)s * g.N + n) * g.ldp + m;
+        float *p = g.partial + (int64_t)s * g.sstride + (int64_t)n * g.ldp + m;
         *reinterpret_cast<f32x4 *>(p) = f32x4{v[0], v[1], v[2], v[3]};
       }
     }
@@ -355,13 +570,96 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(KArgs g) {
   for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
     const int n = (int)(t / m4);
     const int m = (int)(t - (int64_t)n * m4) * 4;
-    f32x4 a = *reinterpret_cast<const f32x4 *>(g.partial + (int64_t)n * g.ldp + m);
-    for (int s = 1; s < g.splits; ++s) {
-      const f32x4 b = *reinterpret_cast<const f32x4 *>(g.partial + ((int64_t)s * g.N + n) * g.ldp + m);
-      a += b;
+    // loads of up to 8 splits are issued together; the adds keep split order
+    const float *p0 = g.partial + (int64_t)n * g.ldp + m;
+    const int64_t sstride = g.sstride;
+    f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < g.splits; s0 += 8) {
+      f32x4 q[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < g.splits) q[u] = *reinterpret_cast<const f32x4 *>(p0 + (s0 + u) * sstride);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < g.splits) a = (s0 + u == 0) ? q[u] : a + q[u];
     }
     const float v[4] = {a[0], a[1], a[2], a[3]};
-    epilogue4(g.epi, g.M, m, n, v, g.out_vec);
+    epilogue4(g, m, n, v);
+  }
+}
+
+// Lean split-K reduction for the epilogues the layer products use (store with optional
+// bias/ReLU, or store with the ReLU mask), 8 outputs per thread on a 2-D grid
+// (blockIdx.y = n). Splits are added in split order, as in the generic kernel.
+template <bool OUT_BF16, bool MASK>
+__global__ void __launch_bounds__(256) splitk_reduce_fast(KArgs g) {
+  const int n = blockIdx.y;
+  const int m = (blockIdx.x * 256 + threadIdx.x) * 8;
+  if (m >= g.M) return;
+  const Epilogue &e = g.epi;
+  const float *p0 = g.partial + (int64_t)n * g.ldp + m;
+  f32x4 a0 = *reinterpret_cast<const f32x4 *>(p0);
+  f32x4 a1 = *reinterpret_cast<const f32x4 *>(p0 + 4);
+  for (int s0 = 1; s0 < g.splits; s0 += 4) {
+    f32x4 q0[4], q1[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (s0 + u < g.splits) {
+        const float *p = p0 + (int64_t)(s0 + u) * g.sstride;
+        q0[u] = *reinterpret_cast<const f32x4 *>(p);
+        q1[u] = *reinterpret_cast<const f32x4 *>(p + 4);
+      }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (s0 + u < g.splits) {
+        a0 += q0[u];
+        a1 += q1[u];
+      }
+  }
+  float x[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+  if (e.bias) {
+    const f32x4 b0 = *reinterpret_cast<const f32x4 *>(e.bias + m);
+    const f32x4 b1 = *reinterpret_cast<const f32x4 *>(e.bias + m + 4);
+    const float bb[8] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = e.alpha * x[i] + bb[i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = e.alpha * x[i];
+  }
+  if (e.relu) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = x[i] > 0.f ? x[i] : 0.f;
+  }
+  if constexpr (MASK) {
+    // mask element type follows the activation type (bf16 here, fp32 for fp32 networks)
+    const int64_t off = (int64_t)n * e.ldmask + m;
+    if (e.mask_dtype == IMBD_BF16) {
+      const u32x4 mk = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint16_t *>(e.mask) + off);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint16_t h = (uint16_t)((mk[i >> 1] >> (16 * (i & 1))) & 0xffffu);
+        if (!(bf16_to_f32(h) > 0.f)) x[i] = 0.f;
+      }
+    } else {
+      const f32x4 m0 = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(e.mask) + off);
+      const f32x4 m1 = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(e.mask) + off + 4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (!(m0[i] > 0.f)) x[i] = 0.f;
+        if (!(m1[i] > 0.f)) x[i + 4] = 0.f;
+      }
+    }
+  }
+  if constexpr (OUT_BF16) {
+    u32x4 pk;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pk[i] = pack_bf16x2(x[2 * i], x[2 * i + 1]);
+    *reinterpret_cast<u32x4 *>(reinterpret_cast<uint16_t *>(e.out) + (int64_t)n * e.ldo + m) = pk;
+  } else {
+    float *o = reinterpret_cast<float *>(e.out) + (int64_t)n * e.ldo + m;
+    *reinterpret_cast<f32x4 *>(o) = f32x4{x[0], x[1], x[2], x[3]};
+    *reinterpret_cast<f32x4 *>(o + 4) = f32x4{x[4], x[5], x[6], x[7]};
   }
 }
 
@@ -401,6 +699,12 @@ int env_int(const char *name, int dflt) {
 
 inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
+// Split-K partial sums: [split][n][ldp] fp32. Row pitch and split pitch are kept off powers
+// of two (+256 B and +4.25 KiB) so the splits of one output do not all map to the same
+// DRAM bank.
+inline int64_t partial_ld(int M) { return ((int64_t)M + 7) / 8 * 8 + 64; }
+inline int64_t partial_split_stride(int M, int N) { return (int64_t)N * partial_ld(M) + 1088; }
+
 }  // namespace
 
 GemmPlan gemm_plan(const GemmProblem &p) {
@@ -434,12 +738,15 @@ GemmPlan gemm_plan(const GemmProblem &p) {
   splits = p.K > 0 ? cdiv(p.K, k_split) : 1;
   pl.splits = splits;
   pl.k_split = k_split;
-  const int64_t ldp = ((int64_t)p.M + 3) / 4 * 4;
-  pl.ws_bytes = splits > 1 ? (size_t)splits * (size_t)p.N * (size_t)ldp * sizeof(float) : 0;
+  pl.ws_bytes = splits > 1 ? (size_t)splits * (size_t)partial_split_stride(p.M, p.N) * sizeof(float) : 0;
   return pl;
 }
 
 int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (p.db_mode != 0 && p.b_kc) {
+    set_error("bias sums need the B operand stored [k][n]");
+    return IMBD_EINVAL;
+  }
   if (p.M <= 0 || p.N <= 0) return IMBD_OK;
   const GemmPlan pl = gemm_plan(p);
   if (pl.splits > 1 && (ws == nullptr || ws_bytes < pl.ws_bytes)) {
@@ -474,9 +781,21 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     if (e.mode == EPI_SGD && e.out2) ok = ok && ((uintptr_t)e.out2 % 8 == 0) && (e.ldo2 % 4 == 0);
     g.out_vec = ok;
   }
+  {
+    const Epilogue &e = p.epi;
+    const int mes = e.mask_dtype == IMBD_BF16 ? 2 : 4;
+    g.mask_vec = e.mask && ((uintptr_t)e.mask % (4 * mes) == 0) && (e.ldmask % 4 == 0);
+    g.bias_vec = e.bias && ((uintptr_t)e.bias % 16 == 0);
+  }
   g.epi = p.epi;
+  g.db_mode = p.db_mode;
+  g.db_out = p.db_out;
+  g.bias = p.bias;
+  g.db_alpha = p.db_alpha;
+  g.bias_lr = p.bias_lr;
   g.partial = reinterpret_cast<float *>(ws);
-  g.ldp = ((int64_t)p.M + 3) / 4 * 4;
+  g.ldp = partial_ld(p.M);
+  g.sstride = partial_split_stride(p.M, p.N);
 
   const TileCfg &c = kCfgs[pl.cfg];
   KernelFn fn = c.fn[p.dtype == IMBD_BF16][p.a_kc][p.b_kc];
@@ -487,12 +806,35 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   }
   int rc = check_launch("gemm");
   if (rc != IMBD_OK) return rc;
+  if (p.db_mode != 0 && pl.splits > 1) {
+    // the in-kernel row sums need the whole K range in one workgroup
+    rc = run_bias_grad(p.dtype, p.N, p.K, p.B, p.ldb, p.db_alpha, p.db_mode == 1 ? p.db_out : nullptr,
+                       p.db_mode == 2 ? p.bias : nullptr, p.bias_lr, s, p.layer);
+    if (rc != IMBD_OK) return rc;
+  }
   if (pl.splits > 1) {
-    const int64_t total = (int64_t)p.N * ((p.M + 3) / 4);
-    int blocks = (int)((total + 255) / 256);
-    if (blocks > 4096) blocks = 4096;
-    {
-      LaunchTimer t(IMBD_K_SPLITK, p.layer, s);
+    // the lean kernel needs 8-aligned rows (M, ld and pointers) and a store epilogue
+    const Epilogue &e = p.epi;
+    const int oes = e.out_dtype == IMBD_BF16 ? 2 : 4;
+    const bool lean = e.mode == EPI_STORE && p.M % 8 == 0 && e.ldo % 8 == 0 && (uintptr_t)e.out % (8 * oes) == 0 &&
+                      (!e.bias || (uintptr_t)e.bias % 32 == 0) &&
+                      (!e.mask || (e.ldmask % 8 == 0 && (uintptr_t)e.mask % (e.mask_dtype == IMBD_BF16 ? 16 : 32) == 0)) &&
+                      g.ldp % 8 == 0 && g.sstride % 8 == 0 && p.N <= 65535;
+    LaunchTimer t(IMBD_K_SPLITK, p.layer, s);
+    if (lean) {
+      const dim3 grid((unsigned)((p.M / 8 + 255) / 256), (unsigned)p.N);
+      const bool bf = e.out_dtype == IMBD_BF16;
+      if (e.mask) {
+        if (bf) hipLaunchKernelGGL((splitk_reduce_fast<true, true>), grid, dim3(256), 0, s, g);
+        else hipLaunchKernelGGL((splitk_reduce_fast<false, true>), grid, dim3(256), 0, s, g);
+      } else {
+        if (bf) hipLaunchKernelGGL((splitk_reduce_fast<true, false>), grid, dim3(256), 0, s, g);
+        else hipLaunchKernelGGL((splitk_reduce_fast<false, false>), grid, dim3(256), 0, s, g);
+      }
+    } else {
+      const int64_t total = (int64_t)p.N * ((p.M + 3) / 4);
+      int blocks = (int)((total + 255) / 256);
+      if (blocks > 4096) blocks = 4096;
       hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, g);
     }
     rc = check_launch("splitk_reduce");

@@ -21,7 +21,10 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // One wave per sample row: row maximum, sum of exp(z - max), per-sample loss
-// lse - z[label] and the gradient inv_batch * (softmax - onehot).
+// lse - z[label] and the gradient inv_batch * (softmax - onehot). NPL > 0 keeps the row in
+// registers (NPL values per lane, C <= 64*NPL) so the logits are read once; NPL == 0 reads
+// them from memory in each pass (any C).
+template <int NPL>
 __global__ void __launch_bounds__(256)
     softmax_xent_rows(int B, int C, const float *__restrict__ Z, int64_t ldz,
                       const int32_t *__restrict__ labels, float inv_batch,
@@ -30,20 +33,47 @@ __global__ void __launch_bounds__(256)
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= B) return;
   const float *z = Z + (int64_t)row * ldz;
-  float mx = -INFINITY;
-  for (int c = lane; c < C; c += 64) mx = fmaxf(mx, z[c]);
-  mx = wave_max(mx);
-  float s = 0.f;
-  for (int c = lane; c < C; c += 64) s += expf(z[c] - mx);
-  s = wave_sum(s);
   const int lab = labels[row];
   const bool ok = lab >= 0 && lab < C;
+  float mx = -INFINITY, s = 0.f;
+  float v[NPL > 0 ? NPL : 1];
+  if constexpr (NPL > 0) {
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const int c = lane + 64 * j;
+      v[j] = c < C ? z[c] : -INFINITY;
+      mx = fmaxf(mx, v[j]);
+    }
+    mx = wave_max(mx);
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      v[j] = expf(v[j] - mx);   // exp(-inf) = 0 for the padding
+      s += v[j];
+    }
+  } else {
+    for (int c = lane; c < C; c += 64) mx = fmaxf(mx, z[c]);
+    mx = wave_max(mx);
+    for (int c = lane; c < C; c += 64) s += expf(z[c] - mx);
+  }
+  s = wave_sum(s);
   if (lane == 0) row_loss[row] = ok ? (mx + logf(s) - z[lab]) : __builtin_nanf("");
-  if (dz) {
-    const float inv_s = 1.0f / s;
+  if (!dz) return;
+  const float inv_s = 1.0f / s;
+  if constexpr (NPL > 0) {
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const int c = lane + 64 * j;
+      if (c < C) {
+        const float g = inv_batch * (v[j] * inv_s - (c == lab ? 1.0f : 0.0f));
+        if (dz_bf16)
+          reinterpret_cast<uint16_t *>(dz)[(int64_t)row * lddz + c] = f32_to_bf16(g);
+        else
+          reinterpret_cast<float *>(dz)[(int64_t)row * lddz + c] = g;
+      }
+    }
+  } else {
     for (int c = lane; c < C; c += 64) {
-      const float p = expf(z[c] - mx) * inv_s;
-      const float g = inv_batch * (p - (c == lab ? 1.0f : 0.0f));
+      const float g = inv_batch * (expf(z[c] - mx) * inv_s - (c == lab ? 1.0f : 0.0f));
       if (dz_bf16)
         reinterpret_cast<uint16_t *>(dz)[(int64_t)row * lddz + c] = f32_to_bf16(g);
       else
@@ -68,22 +98,33 @@ __global__ void __launch_bounds__(256)
   if (threadIdx.x == 0) *loss = inv_batch * part[0];
 }
 
-// db[m] = alpha * sum_b dy[b][m] in ascending b; optionally bias[m] -= lr * db[m].
+// db[m] = alpha * sum_b dy[b][m]: 64 columns per workgroup, each column's rows split in
+// 4 contiguous slices summed in ascending b, the slice sums added in slice order;
+// optionally bias[m] -= lr * db[m].
 template <typename T>
 __global__ void __launch_bounds__(256)
     bias_grad_kernel(int M, int B, const T *__restrict__ dy, int64_t lddy, float alpha,
                      float *__restrict__ db_out, float *__restrict__ bias, float lr) {
-  const int m = blockIdx.x * 256 + threadIdx.x;
-  if (m >= M) return;
+  __shared__ float part[4][64];
+  const int col = threadIdx.x & 63, slice = threadIdx.x >> 6;
+  const int m = blockIdx.x * 64 + col;
+  const int per = (B + 3) / 4;
+  const int b0 = slice * per, b1 = min(B, b0 + per);
   float s = 0.f;
-  for (int b = 0; b < B; ++b) {
-    const T v = dy[(int64_t)b * lddy + m];
-    if constexpr (sizeof(T) == 2) s += bf16_to_f32(v);
-    else s += v;
+  if (m < M) {
+    for (int b = b0; b < b1; ++b) {
+      const T v = dy[(int64_t)b * lddy + m];
+      if constexpr (sizeof(T) == 2) s += bf16_to_f32(v);
+      else s += v;
+    }
   }
-  const float g = alpha * s;
-  if (db_out) db_out[m] = g;
-  if (bias) bias[m] = fmaf(-lr, g, bias[m]);
+  part[slice][col] = s;
+  __syncthreads();
+  if (slice == 0 && m < M) {
+    const float g = alpha * (((part[0][col] + part[1][col]) + part[2][col]) + part[3][col]);
+    if (db_out) db_out[m] = g;
+    if (bias) bias[m] = fmaf(-lr, g, bias[m]);
+  }
 }
 
 // w <- w - step * g (one fp32 rounding), optional bf16 copy. Four elements per thread.
@@ -147,8 +188,17 @@ int run_softmax_xent(int B, int C, const float *logits, int64_t ldz, const int32
   if (B <= 0) return IMBD_OK;
   {
     LaunchTimer t(IMBD_K_SOFTMAX, layer, s);
-    hipLaunchKernelGGL(softmax_xent_rows, dim3((B + 3) / 4), dim3(256), 0, s, B, C, logits, ldz,
-                       labels, inv_batch, row_loss, dz, lddz, dz_dtype == IMBD_BF16 ? 1 : 0);
+    const int bf = dz_dtype == IMBD_BF16 ? 1 : 0;
+    const dim3 grid((B + 3) / 4);
+    if (C <= 64 * 4)
+      hipLaunchKernelGGL(softmax_xent_rows<4>, grid, dim3(256), 0, s, B, C, logits, ldz, labels, inv_batch,
+                         row_loss, dz, lddz, bf);
+    else if (C <= 64 * 16)
+      hipLaunchKernelGGL(softmax_xent_rows<16>, grid, dim3(256), 0, s, B, C, logits, ldz, labels, inv_batch,
+                         row_loss, dz, lddz, bf);
+    else
+      hipLaunchKernelGGL(softmax_xent_rows<0>, grid, dim3(256), 0, s, B, C, logits, ldz, labels, inv_batch,
+                         row_loss, dz, lddz, bf);
   }
   int rc = check_launch("softmax_xent_rows");
   if (rc) return rc;
@@ -161,10 +211,10 @@ int run_bias_grad(int dtype, int M, int B, const void *dy, int64_t lddy, float a
   if (M <= 0) return IMBD_OK;
   LaunchTimer t(IMBD_K_BIAS, layer, s);
   if (dtype == IMBD_BF16)
-    hipLaunchKernelGGL(bias_grad_kernel<uint16_t>, dim3((M + 255) / 256), dim3(256), 0, s, M, B,
+    hipLaunchKernelGGL(bias_grad_kernel<uint16_t>, dim3((M + 63) / 64), dim3(256), 0, s, M, B,
                        reinterpret_cast<const uint16_t *>(dy), lddy, alpha, db_out, bias_sgd, lr);
   else
-    hipLaunchKernelGGL(bias_grad_kernel<float>, dim3((M + 255) / 256), dim3(256), 0, s, M, B,
+    hipLaunchKernelGGL(bias_grad_kernel<float>, dim3((M + 63) / 64), dim3(256), 0, s, M, B,
                        reinterpret_cast<const float *>(dy), lddy, alpha, db_out, bias_sgd, lr);
   return check_launch("bias_grad");
 }
