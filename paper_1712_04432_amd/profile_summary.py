@@ -26,8 +26,9 @@ def summarize(path: str):
     rows = list(csv.DictReader(open(path)))
     groups = collections.defaultdict(list)
     for r in rows:
-        wg = int(r["Workgroup_Size_X"])
-        grid = int(r["Grid_Size_X"]) // max(wg, 1)
+        wg = int(r["Workgroup_Size_X"]) * int(r.get("Workgroup_Size_Y", 1) or 1) * int(r.get("Workgroup_Size_Z", 1) or 1)
+        items = int(r["Grid_Size_X"]) * int(r.get("Grid_Size_Y", 1) or 1) * int(r.get("Grid_Size_Z", 1) or 1)
+        grid = items // max(wg, 1)
         dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0
         groups[(short_name(r["Kernel_Name"]), grid, wg)].append(dur)
     total = sum(sum(v) for v in groups.values())
