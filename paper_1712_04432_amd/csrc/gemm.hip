@@ -52,6 +52,11 @@ __device__ __forceinline__ u32x4 load16(const T *p, int valid, bool vec_ok) {
   return r;
 }
 
+// Padded-grid geometry for masked k rows (convolution weight gradient).
+struct KMask {
+  int wp = 1, hp = 1, w = 1, h = 1;
+};
+
 // Operand with k contiguous in memory: the tile is R rows x 128 bytes, 8 chunks per row.
 template <typename T, int R, int NT>
 struct KcLoader {
@@ -61,9 +66,9 @@ struct KcLoader {
   u32x4 v[PER];
 
   // G: guarded (edge tile: masked, possibly unaligned); !G: interior tile, plain loads
-  template <bool G>
+  template <bool G, bool KM = false>
   __device__ __forceinline__ void load(const T *base, int64_t ld, int row0, int rows, int k0,
-                                       int kend, bool vec_ok, int tid) {
+                                       int kend, bool vec_ok, int tid, KMask = KMask{}) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = tid + i * NT;
@@ -104,24 +109,43 @@ struct TrLoader {
   static constexpr int PER = (NB + NT - 1) / NT;
   u32x4 v[PER][VEC];
 
-  template <bool G>
+  // KM: k indexes positions of a zero-padded (hp x wp) image grid; rows whose position
+  // falls outside the inner (h x w) image read as zero.
+  template <bool G, bool KM = false>
   __device__ __forceinline__ void load(const T *base, int64_t ld, int row0, int rows, int k0,
-                                       int kend, bool vec_ok, int tid) {
+                                       int kend, bool vec_ok, int tid, KMask km = KMask{}) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int blk = tid + i * NT;
       if (NB % NT == 0 || blk < NB) {
         const int kb = blk & 7, rb = blk >> 3;
         const int col = row0 + rb * VEC;
+        int wpos = 0, hpos = 0;
+        if constexpr (KM) {
+          const int kf = k0 + kb * VEC;
+          const int q = kf / km.wp;
+          wpos = kf - q * km.wp;
+          hpos = q % km.hp;
+        }
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
           const int k = k0 + kb * VEC + j;
           const T *p = base + (int64_t)k * ld + col;
+          bool inside = true;
+          if constexpr (KM) {
+            int w = wpos + j, h = hpos;
+            if (w >= km.wp) {  // VEC < wp: at most one wrap into the next grid row
+              w -= km.wp;
+              h = (h + 1 == km.hp) ? 0 : h + 1;
+            }
+            inside = (w < km.w) && (h < km.h);
+          }
           if constexpr (G) {
-            const int valid = (k < kend) ? (rows - col) : 0;
+            const int valid = (k < kend && inside) ? (rows - col) : 0;
             v[i][j] = load16<T>(p, valid, vec_ok);
           } else {
-            v[i][j] = *reinterpret_cast<const u32x4 *>(p);
+            const u32x4 x = *reinterpret_cast<const u32x4 *>(p);
+            v[i][j] = inside ? x : u32x4{0u, 0u, 0u, 0u};
           }
         }
       }
@@ -185,6 +209,7 @@ struct KArgs {
   float *db_out;
   float *bias;
   float db_alpha, bias_lr;
+  int cH, cW, cCi, cCo;  // 3x3 conv tile geometry (conv launches only)
 };
 
 // ------------------------------------------------------------------------- epilogue
@@ -218,11 +243,13 @@ __device__ __forceinline__ void epilogue4(const KArgs &g, int m, int n, const fl
         *reinterpret_cast<u32x2 *>(e.out2 + (int64_t)n * e.ldo2 + m) = pk;
       }
     } else {
-      for (int i = 0; i < cnt; ++i) {
-        const float nw = fmaf(-e.lr, e.alpha * v[i], w[i]);
-        w[i] = nw;
-        if (e.out2) e.out2[(int64_t)n * e.ldo2 + m + i] = f32_to_bf16(nw);
-      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < cnt) {
+          const float nw = fmaf(-e.lr, e.alpha * v[i], w[i]);
+          w[i] = nw;
+          if (e.out2) e.out2[(int64_t)n * e.ldo2 + m + i] = f32_to_bf16(nw);
+        }
     }
     return;
   }
@@ -232,7 +259,9 @@ __device__ __forceinline__ void epilogue4(const KArgs &g, int m, int n, const fl
       const f32x4 b4 = *reinterpret_cast<const f32x4 *>(e.bias + m);
       bias[0] = b4[0]; bias[1] = b4[1]; bias[2] = b4[2]; bias[3] = b4[3];
     } else {
-      for (int i = 0; i < cnt; ++i) bias[i] = e.bias[m + i];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < cnt) bias[i] = e.bias[m + i];
     }
   }
   if (e.mask) {
@@ -250,7 +279,9 @@ __device__ __forceinline__ void epilogue4(const KArgs &g, int m, int n, const fl
         for (int i = 0; i < 4; ++i) keep[i] = mk[i] > 0.f;
       }
     } else {
-      for (int i = 0; i < cnt; ++i) keep[i] = mask_at(e, m + i, n) > 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < cnt) keep[i] = mask_at(e, m + i, n) > 0.f;
     }
   }
 #pragma unroll
@@ -267,20 +298,39 @@ __device__ __forceinline__ void epilogue4(const KArgs &g, int m, int n, const fl
       pk[1] = pack_bf16x2(x[2], x[3]);
       *reinterpret_cast<u32x2 *>(o) = pk;
     } else {
-      for (int i = 0; i < cnt; ++i) o[i] = f32_to_bf16(x[i]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < cnt) o[i] = f32_to_bf16(x[i]);
     }
   } else {
     float *o = reinterpret_cast<float *>(e.out) + (int64_t)n * e.ldo + m;
     if (vec) {
       *reinterpret_cast<f32x4 *>(o) = f32x4{x[0], x[1], x[2], x[3]};
     } else {
-      for (int i = 0; i < cnt; ++i) o[i] = x[i];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < cnt) o[i] = x[i];
     }
   }
 }
 
+// Position P of the padded grid (n, h, w) -> output pixel row (n*H + h)*W + w, or -1 when
+// (h, w) lies in the padding (those positions are computed and dropped).
+__device__ __forceinline__ int conv_out_row(const KArgs &g, int P) {
+  const int Wp = g.cW + 2, Hp = g.cH + 2;
+  const int n = P / (Hp * Wp);
+  const int rem = P - n * Hp * Wp;
+  const int h = rem / Wp;
+  const int w = rem - h * Wp;
+  if (h >= g.cH || w >= g.cW) return -1;
+  return (n * g.cH + h) * g.cW + w;
+}
+
 // --------------------------------------------------------------------------- kernel
-template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, bool A_KC, bool B_KC>
+// CONV selects how operands are addressed: 0 plain matrices; 1/2/3 the forward, input-
+// gradient and weight-gradient passes of a 3x3 conv tile, computed on the positions of
+// the zero-padded (H+2) x (W+2) grid so that every tap is a row shift of a dense matrix.
+template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, bool A_KC, bool B_KC, int CONV = 0>
 __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
     gemm_kernel(KArgs g) {
   constexpr int NT = 64 * WAVES_M * WAVES_N;
@@ -297,7 +347,7 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
   // The weight-gradient product (both operands strided) is the one that carries the
   // fused update; its old master tile is fetched before the K loop so the read half of
   // the read-modify-write overlaps the products.
-  constexpr bool PREFETCH_W = !A_KC && !B_KC;
+  constexpr bool PREFETCH_W = !A_KC && !B_KC && CONV == 0;
   // Row sums of the B tile (the bias gradient), NT/BN threads per row.
   constexpr int TPR = NT / BN;
   constexpr int CPT = 8 / TPR;  // 16-byte chunks per thread per K tile
@@ -428,36 +478,84 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
   };
   auto buf = [&](int kt) { return smem + (kt & 1) * STAGE; };
 
+  // Operand sources of K tile kt of this split.
+  const int Wp = g.cW + 2;
+  const T *A_rs = A;
+  if constexpr (CONV == 3) {
+    // rows of A are m = tap*C_in + c; a tile lies within one tap (C_in % BM == 0)
+    const int rs = m0 / g.cCi, r = rs / 3, sx = rs - 3 * r;
+    A_rs = A + (int64_t)(r * Wp + sx - rs) * g.cCi;
+  }
+  KMask km;
+  if constexpr (CONV == 3) {
+    km.wp = Wp;
+    km.hp = g.cH + 2;
+    km.w = g.cW;
+    km.h = g.cH;
+  }
+  auto issueA = [&](auto &L, int kt, auto gtag) {
+    constexpr bool G = decltype(gtag)::value;
+    const int kg = kbeg + kt * BK;
+    if constexpr (CONV == 2) {
+      // W[o][tap][c] read as A(c, o) for one tap
+      const int rs = kg / g.cCo, o0 = kg - rs * g.cCo;
+      L.template load<G>(A + (int64_t)rs * g.cCi, g.lda, m0, g.M, o0, g.cCo, g.a_vec, tid);
+    } else {
+      L.template load<G>(A_rs, g.lda, m0, g.M, kg, kend, g.a_vec, tid);
+    }
+  };
+  auto issueB = [&](auto &L, int kt, auto gtag) {
+    constexpr bool G = decltype(gtag)::value;
+    const int kg = kbeg + kt * BK;
+    if constexpr (CONV == 1) {
+      // x_pad shifted by tap (r, s): B(c, P) = x_pad_flat[P + r*Wp + s][c]
+      const int rs = kg / g.cCi, c0 = kg - rs * g.cCi, r = rs / 3, sx = rs - 3 * r;
+      L.template load<G>(Bp + (int64_t)(r * Wp + sx) * g.cCi, g.ldb, n0, g.N, c0, g.cCi, g.b_vec, tid_b);
+    } else if constexpr (CONV == 2) {
+      // dy_pad shifted by (2-r, 2-s): B(o, P) = dy_pad_flat[P + (2-r)*Wp + 2-s][o]
+      const int rs = kg / g.cCo, o0 = kg - rs * g.cCo, r = rs / 3, sx = rs - 3 * r;
+      L.template load<G>(Bp + (int64_t)((2 - r) * Wp + 2 - sx) * g.cCo, g.ldb, n0, g.N, o0, g.cCo, g.b_vec,
+                         tid_b);
+    } else if constexpr (CONV == 3) {
+      // interior of dy_pad, rows outside the inner image masked to zero
+      L.template load<G, true>(Bp, g.ldb, n0, g.N, kg, kend, g.b_vec, tid_b, km);
+    } else {
+      L.template load<G>(Bp, g.ldb, n0, g.N, kg, kend, g.b_vec, tid_b);
+    }
+  };
+  const BoolTag<false> plain{};
+  const BoolTag<true> guarded{};
+
   if (interior) {
-    auto ktile = [&](int kt) { return kbeg + min(kt, nk - 1) * BK; };
-    la[0].template load<false>(A, g.lda, m0, g.M, ktile(0), kend, true, tid);
-    lb[0].template load<false>(Bp, g.ldb, n0, g.N, ktile(0), kend, true, tid_b);
+    auto kc = [&](int kt) { return min(kt, nk - 1); };
+    issueA(la[0], 0, plain);
+    issueB(lb[0], 0, plain);
     la[0].store(buf(0), tid);
     lb[0].store(buf(0) + STAGE_A, tid_b);
     if constexpr (NSTAGE == 2) {
-      la[1].template load<false>(A, g.lda, m0, g.M, ktile(1), kend, true, tid);
-      lb[1].template load<false>(Bp, g.ldb, n0, g.N, ktile(1), kend, true, tid_b);
+      issueA(la[NSTAGE - 1], kc(1), plain);
+      issueB(lb[NSTAGE - 1], kc(1), plain);
     }
     __syncthreads();
     for (int kt = 0; kt < nk; kt += NSTAGE) {
       if constexpr (NSTAGE == 2) {
         // step kt: set 1 holds tile kt+1; set 0 receives tile kt+2
-        la[0].template load<false>(A, g.lda, m0, g.M, ktile(kt + 2), kend, true, tid);
-        lb[0].template load<false>(Bp, g.ldb, n0, g.N, ktile(kt + 2), kend, true, tid_b);
+        issueA(la[0], kc(kt + 2), plain);
+        issueB(lb[0], kc(kt + 2), plain);
         compute(kt);
-        la[1].store(buf(kt + 1), tid);
-        lb[1].store(buf(kt + 1) + STAGE_A, tid_b);
+        la[NSTAGE - 1].store(buf(kt + 1), tid);
+        lb[NSTAGE - 1].store(buf(kt + 1) + STAGE_A, tid_b);
         __syncthreads();
         // step kt+1: set 0 holds tile kt+2; set 1 receives tile kt+3
-        la[1].template load<false>(A, g.lda, m0, g.M, ktile(kt + 3), kend, true, tid);
-        lb[1].template load<false>(Bp, g.ldb, n0, g.N, ktile(kt + 3), kend, true, tid_b);
+        issueA(la[NSTAGE - 1], kc(kt + 3), plain);
+        issueB(lb[NSTAGE - 1], kc(kt + 3), plain);
         compute(kt + 1);
         la[0].store(buf(kt + 2), tid);
         lb[0].store(buf(kt + 2) + STAGE_A, tid_b);
         __syncthreads();
       } else {
-        la[0].template load<false>(A, g.lda, m0, g.M, ktile(kt + 1), kend, true, tid);
-        lb[0].template load<false>(Bp, g.ldb, n0, g.N, ktile(kt + 1), kend, true, tid_b);
+        issueA(la[0], kc(kt + 1), plain);
+        issueB(lb[0], kc(kt + 1), plain);
         compute(kt);
         la[0].store(buf(kt + 1), tid);
         lb[0].store(buf(kt + 1) + STAGE_A, tid_b);
@@ -467,8 +565,8 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
   } else {
     // edge tiles: masked loads, one register stage
     if (nk > 0) {
-      la[0].template load<true>(A, g.lda, m0, g.M, kbeg, kend, g.a_vec, tid);
-      lb[0].template load<true>(Bp, g.ldb, n0, g.N, kbeg, kend, g.b_vec, tid_b);
+      issueA(la[0], 0, guarded);
+      issueB(lb[0], 0, guarded);
       la[0].store(buf(0), tid);
       lb[0].store(buf(0) + STAGE_A, tid_b);
     }
@@ -476,8 +574,8 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
     for (int kt = 0; kt < nk; ++kt) {
       const bool more = kt + 1 < nk;
       if (more) {
-        la[0].template load<true>(A, g.lda, m0, g.M, kbeg + (kt + 1) * BK, kend, g.a_vec, tid);
-        lb[0].template load<true>(Bp, g.ldb, n0, g.N, kbeg + (kt + 1) * BK, kend, g.b_vec, tid_b);
+        issueA(la[0], kt + 1, guarded);
+        issueB(lb[0], kt + 1, guarded);
       }
       compute(kt);
       if (more) {
@@ -517,8 +615,12 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
       const int nl = p * RPP + er;
-      const int n = n0 + nl;
+      int n = n0 + nl;
       const f32x4 a = *reinterpret_cast<const f32x4 *>(stg + nl * PT + ec);
+      if constexpr (CONV == 1 || CONV == 2) {
+        n = conv_out_row(g, n);
+        if (n < 0) continue;
+      }
       if (g.splits > 1) {
         *reinterpret_cast<f32x4 *>(g.partial + (int64_t)s * g.sstride + (int64_t)n * g.ldp + m) = a;
         continue;
@@ -555,7 +657,12 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
       if (m >= g.M || n >= g.N) continue;
       const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
       if (g.splits == 1) {
-        epilogue4(g, m, n, v);
+        int on = n;
+        if constexpr (CONV == 1 || CONV == 2) {
+          on = conv_out_row(g, n);
+          if (on < 0) continue;
+        }
+        epilogue4(g, m, on, v);
       } else {
         float *p = g.partial + (int64_t)s * g.sstride + (int64_t)n * g.ldp + m;
         *reinterpret_cast<f32x4 *>(p) = f32x4{v[0], v[1], v[2], v[3]};
@@ -691,6 +798,13 @@ const TileCfg kCfgs[] = {
     make_cfg<64, 128, 2, 2>(),   // 3: wide
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
+
+// Conv launches (bf16): [cfg 0 = 64x64, cfg 1 = 128x128][pass 1..3]
+const KernelFn kConvFns[2][3] = {
+    {gemm_kernel<uint16_t, 64, 64, 2, 2, true, true, 1>, gemm_kernel<uint16_t, 64, 64, 2, 2, false, true, 2>,
+     gemm_kernel<uint16_t, 64, 64, 2, 2, false, false, 3>},
+    {gemm_kernel<uint16_t, 128, 128, 2, 2, true, true, 1>, gemm_kernel<uint16_t, 128, 128, 2, 2, false, true, 2>,
+     gemm_kernel<uint16_t, 128, 128, 2, 2, false, false, 3>}};
 
 int env_int(const char *name, int dflt) {
   const char *v = getenv(name);
@@ -840,6 +954,128 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     rc = check_launch("splitk_reduce");
   }
   return rc;
+}
+
+// ------------------------------------------------------------------ 3x3 conv tile
+// The three passes of a 3x3, stride-1 conv on a tile whose 1-pixel halo is in place
+// (Sec. 2.2 of the paper, domain parallelism), as implicit GEMMs over the positions P of
+// the padded (H+2) x (W+2) grid. Positions are numbered up to the last interior pixel, so
+// every shifted row stays inside the padded tensors.
+//  pass 1  y[P][o]      = sum_{tap,c} w[o][tap][c] x_pad[P + r*(W+2) + s][c]
+//  pass 2  dx[P][c]     = sum_{tap,o} w[o][tap][c] dy_pad[P + (2-r)*(W+2) + 2-s][o]
+//  pass 3  dw[o][tap][c] = sum_{P inside} dy_pad[P + (W+2) + 1][o] x_pad[P + r*(W+2) + s][c]
+namespace {
+struct ConvPlan {
+  int M, N, K, cfg, bm, bn, splits, k_split;
+  size_t ws_bytes;
+};
+
+ConvPlan conv_plan(int pass, int N, int H, int W, int Ci, int Co) {
+  ConvPlan p{};
+  const int64_t Pext = (int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W;
+  p.M = pass == 1 ? Co : (pass == 2 ? Ci : 9 * Ci);
+  p.N = pass == 3 ? Co : (int)Pext;
+  p.K = pass == 1 ? 9 * Ci : (pass == 2 ? 9 * Co : (int)Pext);
+  // a weight-gradient tile must stay inside one tap (C_in % BM == 0)
+  p.cfg = (Ci % 128 == 0 && Co % 128 == 0 && p.M >= 128 && p.N >= 128) ? 1 : 0;
+  p.bm = p.bn = p.cfg == 1 ? 128 : 64;
+  const int tiles = cdiv(p.M, p.bm) * cdiv(p.N, p.bn);
+  const int BK = 64, ktiles = cdiv(p.K, BK);
+  int splits = 1;
+  if (pass == 3 && tiles < 512 && ktiles >= 16) {
+    splits = cdiv(512, tiles);
+    if (splits > ktiles / 4) splits = ktiles / 4;
+    if (splits < 1) splits = 1;
+  }
+  p.k_split = cdiv(cdiv(p.K, splits), BK) * BK;
+  p.splits = cdiv(p.K, p.k_split);
+  p.ws_bytes = p.splits > 1 ? (size_t)p.splits * (size_t)partial_split_stride(p.M, p.N) * sizeof(float) : 0;
+  return p;
+}
+}  // namespace
+
+size_t conv_wgrad_ws_bytes(int N, int H, int W, int Ci, int Co) {
+  if (Ci % 64 || Co % 64) return 0;
+  return conv_plan(3, N, H, W, Ci, Co).ws_bytes;
+}
+
+static int conv_launch(int pass, int N, int H, int W, int Ci, int Co, const void *A, const void *B, void *out,
+                       int out_dtype, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (Ci % 64 || Co % 64) {
+    set_error("conv tile needs C_in and C_out multiples of 64 (got %d, %d)", Ci, Co);
+    return IMBD_EUNSUPPORTED;
+  }
+  const ConvPlan pl = conv_plan(pass, N, H, W, Ci, Co);
+  if ((int64_t)N * (H + 2) * (W + 2) * (Ci > Co ? Ci : Co) >= ((int64_t)1 << 31)) {
+    set_error("conv tile too large for 32-bit element offsets");
+    return IMBD_EUNSUPPORTED;
+  }
+  if (pl.splits > 1 && (ws == nullptr || ws_bytes < pl.ws_bytes || (uintptr_t)ws % 16)) {
+    set_error("conv weight gradient needs %zu bytes of 16-byte aligned workspace, got %zu", pl.ws_bytes, ws_bytes);
+    return IMBD_EWORKSPACE;
+  }
+  for (const void *p : {A, B, (const void *)out})
+    if ((uintptr_t)p % 16) {
+      set_error("conv tensors must be 16-byte aligned");
+      return IMBD_EINVAL;
+    }
+  KArgs g{};
+  g.A = A;
+  g.B = pass == 3 ? (const void *)(reinterpret_cast<const uint16_t *>(B) + (int64_t)(W + 3) * Co) : B;
+  g.lda = pass == 3 ? Ci : 9 * Ci;
+  g.ldb = pass == 1 ? Ci : Co;
+  g.M = pl.M;
+  g.N = pl.N;
+  g.K = pl.K;
+  g.k_split = pl.k_split;
+  g.splits = pl.splits;
+  g.tiles_m = cdiv(pl.M, pl.bm);
+  g.tiles_n = cdiv(pl.N, pl.bn);
+  g.a_vec = g.b_vec = 1;
+  g.out_vec = 1;
+  g.mask_vec = g.bias_vec = 0;
+  g.epi = Epilogue{};
+  g.epi.mode = EPI_STORE;
+  g.epi.out = out;
+  g.epi.out_dtype = pass == 3 ? IMBD_F32 : out_dtype;
+  g.epi.ldo = pass == 1 ? Co : (pass == 2 ? Ci : 9 * Ci);
+  g.partial = reinterpret_cast<float *>(ws);
+  g.ldp = partial_ld(pl.M);
+  g.sstride = partial_split_stride(pl.M, pl.N);
+  g.cH = H;
+  g.cW = W;
+  g.cCi = Ci;
+  g.cCo = Co;
+  const int cls = pass == 1 ? IMBD_K_CONV_FWD : (pass == 2 ? IMBD_K_CONV_DGRAD : IMBD_K_CONV_WGRAD);
+  {
+    LaunchTimer t(cls, 0, s);
+    hipLaunchKernelGGL(kConvFns[pl.cfg][pass - 1], dim3(g.tiles_m * g.tiles_n * g.splits), dim3(256), 0, s, g);
+  }
+  int rc = check_launch("conv3x3");
+  if (rc != IMBD_OK || pl.splits == 1) return rc;
+  {
+    LaunchTimer t(IMBD_K_SPLITK, 0, s);
+    const dim3 grid((unsigned)((pl.M / 8 + 255) / 256), (unsigned)pl.N);
+    hipLaunchKernelGGL((splitk_reduce_fast<false, false>), grid, dim3(256), 0, s, g);
+  }
+  return check_launch("conv3x3 reduce");
+}
+
+int run_conv_fwd(int N, int H, int W, int Ci, int Co, const void *xp, const void *w, void *y, int y_dtype,
+                 hipStream_t s) {
+  return conv_launch(1, N, H, W, Ci, Co, w, xp, y, y_dtype, nullptr, 0, s);
+}
+int run_conv_dgrad(int N, int H, int W, int Ci, int Co, const void *dyp, const void *w, void *dx, int dx_dtype,
+                   hipStream_t s) {
+  return conv_launch(2, N, H, W, Ci, Co, w, dyp, dx, dx_dtype, nullptr, 0, s);
+}
+int run_conv_wgrad(int N, int H, int W, int Ci, int Co, const void *xp, const void *dyp, float *dw, void *ws,
+                   size_t ws_bytes, hipStream_t s) {
+  if (N == 0) {  // an empty tile contributes a zero partial
+    if (hipMemsetAsync(dw, 0, (size_t)Co * 9 * Ci * sizeof(float), s) != hipSuccess) return check_launch("memset");
+    return IMBD_OK;
+  }
+  return conv_launch(3, N, H, W, Ci, Co, xp, dyp, dw, IMBD_F32, ws, ws_bytes, s);
 }
 
 }  // namespace imbd

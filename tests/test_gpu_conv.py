@@ -1,0 +1,141 @@
+"""Parity of the domain-parallel 3x3 conv tile (Sec. 2.2 of the paper) against the oracle.
+
+bf16 operands with the halo in place; outputs compared normwise: fp32 outputs at 1e-5
+(identical operand bits, only fp32 accumulation differs), bf16 outputs at the 2e-2 bar
+(and one bf16 rounding, 2^-8). Full-size tiles (32 x 56 x 56, 256 -> 256) are checked on
+sampled outputs that the oracle computes one by one."""
+import numpy as np
+import pytest
+
+import oracle
+from synthdata import make_conv_inputs
+from tests._util import TOL_BF16, bf16_values, dev_bf16_bits, host, nrm_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _flush(msg):
+    print(msg, flush=True)
+
+
+def _run(imbd, dev, d, out_bf16=False):
+    import torch
+    x = dev_bf16_bits(d["x_bits"], dev)
+    w = dev_bf16_bits(d["w_bits"], dev)
+    dy = dev_bf16_bits(d["dy_bits"], dev)
+    N, Hp, Wp, Ci = x.shape
+    Co = w.shape[0]
+    H, W = Hp - 2, Wp - 2
+    odt = torch.bfloat16 if out_bf16 else torch.float32
+    y = torch.full((N, H, W, Co), float("nan"), dtype=odt, device=dev)
+    dx = torch.full((N, H, W, Ci), float("nan"), dtype=odt, device=dev)
+    dw = torch.full((Co, 3, 3, Ci), float("nan"), device=dev)
+    nws = imbd.conv3x3_wgrad_workspace_bytes(N, H, W, Ci, Co)
+    ws = torch.zeros(max(nws, 16), dtype=torch.uint8, device=dev)
+    imbd.conv3x3_tile_fwd(x, w, y)
+    imbd.conv3x3_tile_dgrad(dy, w, dx)
+    imbd.conv3x3_tile_wgrad(x, dy, dw, ws=ws)
+    torch.cuda.synchronize()
+    return y, dx, dw
+
+
+@pytest.mark.parametrize("N,H,W,Ci,Co", [(2, 5, 7, 64, 128), (1, 9, 4, 128, 64), (2, 6, 6, 128, 128),
+                                         (1, 1, 1, 64, 64), (3, 11, 13, 64, 64)])
+@pytest.mark.parametrize("border", [(False, False, False, False), (True, False, True, False),
+                                    (True, True, True, True)])
+def test_conv_tile_small(imbd, dev, N, H, W, Ci, Co, border):
+    _flush(f"conv small {(N, H, W, Ci, Co)} border={border}")
+    d = make_conv_inputs(N, H, W, Ci, Co, seed=H * 100 + W, border=border)
+    xv, wv, dyv = bf16_values(d["x_bits"]), bf16_values(d["w_bits"]), bf16_values(d["dy_bits"])
+    y, dx, dw = _run(imbd, dev, d)
+    assert nrm_err(host(y), oracle.conv3x3_fwd(xv, wv)) < 1e-5
+    assert nrm_err(host(dx), oracle.conv3x3_dgrad(dyv, wv)) < 1e-5
+    assert nrm_err(host(dw), oracle.conv3x3_wgrad(xv, dyv)) < 1e-5
+    y16, dx16, _ = _run(imbd, dev, d, out_bf16=True)
+    assert nrm_err(host(y16), oracle.conv3x3_fwd(xv, wv)) < 2.0 ** -8
+    assert nrm_err(host(dx16), oracle.conv3x3_dgrad(dyv, wv)) < 2.0 ** -8
+
+
+@pytest.mark.parametrize("border", [(False, False, False, False), (True, False, True, False)])
+def test_conv_tile_full_size_sampled(imbd, dev, border):
+    """The 56x56 tile of a 224x224 image split 4x4, batch 32, 256 -> 256 channels:
+    an interior tile and a corner tile (zero halo on two sides)."""
+    _flush(f"conv full size border={border}")
+    N, H, W, C = 32, 56, 56, 256
+    d = make_conv_inputs(N, H, W, C, C, seed=5, border=border)
+    xv, wv, dyv = bf16_values(d["x_bits"]), bf16_values(d["w_bits"]), bf16_values(d["dy_bits"])
+    y, dx, dw = _run(imbd, dev, d)
+    rng = np.random.default_rng(1)
+    # include the tile's corners and edges among the samples
+    yi = np.concatenate([rng.choice(y.numel(), 200, replace=False),
+                         [0, C - 1, (W - 1) * C, ((H - 1) * W) * C + 3, y.numel() - 1]])
+    assert nrm_err(host(y).reshape(-1)[yi], oracle.conv3x3_fwd_at(xv, wv, yi)) < 1e-5
+    xi = np.concatenate([rng.choice(dx.numel(), 200, replace=False), [0, dx.numel() - 1]])
+    assert nrm_err(host(dx).reshape(-1)[xi], oracle.conv3x3_dgrad_at(dyv, wv, xi)) < 1e-5
+    wi = rng.choice(dw.numel(), 24, replace=False)
+    assert nrm_err(host(dw).reshape(-1)[wi], oracle.conv3x3_wgrad_at(xv, dyv, wi)) < 1e-5
+    # every output written (no NaN left from the fill) and finite
+    import torch
+    assert torch.isfinite(y).all().item() and torch.isfinite(dx).all().item() and torch.isfinite(dw).all().item()
+
+
+def test_conv_stitched_domain_split(imbd, dev):
+    """Domain parallelism on one GPU: a 2x2 split of a zero-padded image with exchanged
+    halos (cut from the full padded tensor) reproduces the full-image conv, the summed
+    weight gradient and the full input gradient (the halo exchange and the all-reduce of
+    Eq. (7) done in software)."""
+    import torch
+    from synthdata import to_bf16_bits
+    rng = np.random.default_rng(2)
+    N, H, W, Ci, Co = 2, 12, 10, 64, 64
+    x = to_bf16_bits(rng.standard_normal((N, H, W, Ci)).astype(np.float32))
+    dy = to_bf16_bits(rng.standard_normal((N, H, W, Co)).astype(np.float32))
+    wt = to_bf16_bits((rng.standard_normal((Co, 3, 3, Ci)) * 0.05).astype(np.float32))
+    xp = np.pad(bf16_values(x), ((0, 0), (1, 1), (1, 1), (0, 0)))
+    dyp = np.pad(bf16_values(dy), ((0, 0), (1, 1), (1, 1), (0, 0)))
+    wv = bf16_values(wt)
+    y_full, dx_full, dw_full = oracle.conv3x3_fwd(xp, wv), oracle.conv3x3_dgrad(dyp, wv), oracle.conv3x3_wgrad(xp, dyp)
+    wd = dev_bf16_bits(wt, dev)
+    th, tw = H // 2, W // 2
+    y = np.zeros_like(y_full)
+    dx = np.zeros_like(dx_full)
+    dw = np.zeros_like(dw_full)
+    for ti in range(2):
+        for tj in range(2):
+            hs, ws_ = ti * th, tj * tw
+            xt = to_bf16_bits(xp[:, hs:hs + th + 2, ws_:ws_ + tw + 2].astype(np.float32))
+            dyt = to_bf16_bits(dyp[:, hs:hs + th + 2, ws_:ws_ + tw + 2].astype(np.float32))
+            xd, dyd = dev_bf16_bits(xt, dev), dev_bf16_bits(dyt, dev)
+            yt = torch.empty((N, th, tw, Co), device=dev)
+            dxt = torch.empty((N, th, tw, Ci), device=dev)
+            dwt = torch.empty((Co, 3, 3, Ci), device=dev)
+            nws = imbd.conv3x3_wgrad_workspace_bytes(N, th, tw, Ci, Co)
+            wsb = torch.zeros(max(nws, 16), dtype=torch.uint8, device=dev)
+            imbd.conv3x3_tile_fwd(xd, wd, yt)
+            imbd.conv3x3_tile_dgrad(dyd, wd, dxt)
+            imbd.conv3x3_tile_wgrad(xd, dyd, dwt, ws=wsb)
+            torch.cuda.synchronize()
+            y[:, hs:hs + th, ws_:ws_ + tw] = host(yt)
+            dx[:, hs:hs + th, ws_:ws_ + tw] = host(dxt)
+            dw += host(dwt)
+    assert nrm_err(y, y_full) < 1e-5
+    assert nrm_err(dx, dx_full) < 1e-5
+    assert nrm_err(dw, dw_full) < 1e-5
+
+
+def test_conv_errors(imbd, dev):
+    import torch
+    x = torch.zeros((1, 4, 4, 48), dtype=torch.bfloat16, device=dev)
+    w = torch.zeros((64, 3, 3, 48), dtype=torch.bfloat16, device=dev)
+    y = torch.zeros((1, 2, 2, 64), device=dev)
+    with pytest.raises(imbd.ImbdError) as e:
+        imbd.conv3x3_tile_fwd(x, w, y)               # C_in not a multiple of 64
+    assert e.value.status == imbd.IMBD_EUNSUPPORTED
+    d = make_conv_inputs(32, 56, 56, 256, 256, seed=0)
+    xd, dyd = dev_bf16_bits(d["x_bits"], dev), dev_bf16_bits(d["dy_bits"], dev)
+    dw = torch.zeros((256, 3, 3, 256), device=dev)
+    assert imbd.conv3x3_wgrad_workspace_bytes(32, 56, 56, 256, 256) > 0
+    with pytest.raises(imbd.ImbdError) as e:
+        imbd.conv3x3_tile_wgrad(xd, dyd, dw, ws=torch.zeros(64, dtype=torch.uint8, device=dev))
+    assert e.value.status == imbd.IMBD_EWORKSPACE
+    torch.cuda.synchronize()
