@@ -11,6 +11,7 @@ weight-gradient kernel with the fused update, timed with HIP events inside the t
 region's twin) and the CPU oracle timed on a bounded sample of the same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+(--workload conv3x3_tile measures the domain-parallel conv tile instead of the FC step)
 """
 from __future__ import annotations
 
@@ -89,6 +90,99 @@ def cpu_baseline(cfg, sample_batch: int = 8):
                       f"{dt:.2f} s = {sample_batch / dt:.3f} samples/s"}
 
 
+def conv_cpu_baseline(cfg, images: int = 8):
+    """The oracle's three conv passes on `images` of the tile's images."""
+    import numpy as np
+
+    import oracle
+    from synthdata import bf16_bits_to_f32, make_conv_inputs
+    d = make_conv_inputs(images, cfg.tile_h, cfg.tile_w, cfg.c_in, cfg.c_out, seed=0)
+    xv = bf16_bits_to_f32(d["x_bits"]).astype(np.float64)
+    wv = bf16_bits_to_f32(d["w_bits"]).astype(np.float64)
+    dyv = bf16_bits_to_f32(d["dy_bits"]).astype(np.float64)
+    t0 = time.perf_counter()
+    oracle.conv3x3_fwd(xv, wv)
+    oracle.conv3x3_dgrad(dyv, wv)
+    oracle.conv3x3_wgrad(xv, dyv)
+    dt = time.perf_counter() - t0
+    flops = 3 * 2 * images * cfg.tile_h * cfg.tile_w * cfg.c_out * 9 * cfg.c_in
+    return {"value": round(flops / dt / 1e12, 9), "unit": "TFLOP/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"forward + input gradient + weight gradient of the 3x3 tile on {images} of the "
+                      f"{cfg.batch} images, fp64 oracle, {dt:.2f} s"}
+
+
+def bench_conv(args):
+    """Domain-parallel conv tile: forward + input gradient + weight gradient per step."""
+    import numpy as np
+    import torch
+
+    import paper_1712_04432_amd as m
+    from synthdata import get_config, make_conv_inputs
+
+    m.load()
+    cfg = get_config("conv3x3_tile")
+    dev = torch.device("cuda:0")
+    N, H, W, Ci, Co = cfg.batch, cfg.tile_h, cfg.tile_w, cfg.c_in, cfg.c_out
+    log(f"bench: conv tile {N}x{H}x{W}, {Ci}->{Co}")
+    d = make_conv_inputs(N, H, W, Ci, Co, seed=0)
+    as_bf16 = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    x, w, dy = as_bf16(d["x_bits"]), as_bf16(d["w_bits"]), as_bf16(d["dy_bits"])
+    y = torch.empty((N, H, W, Co), dtype=torch.bfloat16, device=dev)
+    dx = torch.empty((N, H, W, Ci), dtype=torch.bfloat16, device=dev)
+    dw = torch.empty((Co, 3, 3, Ci), device=dev)
+    ws = torch.zeros(max(m.conv3x3_wgrad_workspace_bytes(N, H, W, Ci, Co), 16), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        m.conv3x3_tile_fwd(x, w, y, stream=stream)
+        m.conv3x3_tile_dgrad(dy, w, dx, stream=stream)
+        m.conv3x3_tile_wgrad(x, dy, dw, ws=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / args.steps
+    per_pass = 2 * N * H * W * Co * 9 * Ci
+    flops = 3 * per_pass
+    tflops = flops / (ms_step * 1e-3) / 1e12
+    kinfo = {}
+    for name, cls in (("forward", m.IMBD_K_CONV_FWD), ("input_grad", m.IMBD_K_CONV_DGRAD),
+                      ("weight_grad", m.IMBD_K_CONV_WGRAD)):
+        m.timing_begin(cls, -1, args.steps)
+        for _ in range(args.steps):
+            step()
+        n, kms = m.timing_end()
+        kinfo[name] = kms / max(n, 1)
+    torch.cuda.synchronize()
+    dom = max(kinfo, key=kinfo.get)
+    achieved = per_pass / (kinfo[dom] * 1e-3) / 1e12
+    result = {
+        "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations and gradients, N(0, 2/(9*256)) weights)",
+        "config": {"workload": f"conv3x3_tile: 3x3 stride-1 conv, {Ci}->{Co} channels, {H}x{W} tile of a "
+                               f"224x224 image split 4x4, 1-pixel halo supplied, batch {N}; forward + input "
+                               f"gradient + weight gradient", "global_batch": N, "parallelism": "single GPU"},
+        "samples_per_s": round(N / (ms_step * 1e-3), 1),
+        "pct_bf16_mfma_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 3),
+        "gflop_per_step": round(flops / 1e9, 4),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "kernel": f"conv tile {dom} pass", "algorithmic_flops_per_launch": per_pass,
+                     "avg_launch_ms": {k: round(v, 5) for k, v in kinfo.items()}},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = conv_cpu_baseline(cfg)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -102,6 +196,9 @@ def main():
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
               f"1.5D grid is not part of it", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "conv3x3_tile":
+        return bench_conv(args)
 
     import numpy as np
     import torch

@@ -76,12 +76,16 @@ struct KcLoader {
         const int r = c >> 3, kc = c & 7;
         const int grow = row0 + r;
         const int kk = k0 + kc * VEC;
-        const T *p = base + (int64_t)grow * ld + kk;
         if constexpr (G) {
           const int valid = (grow < rows) ? (kend - kk) : 0;
-          v[i] = load16<T>(p, valid, vec_ok);
+          v[i] = load16<T>(base + (int64_t)grow * ld + kk, valid, vec_ok);
         } else {
-          v[i] = *reinterpret_cast<const u32x4 *>(p);
+          // fast path: chunks are whole (kend % VEC == 0); out-of-range chunks load a
+          // clamped in-range address and are zeroed, without a branch
+          const bool ok = grow < rows && kk < kend;
+          const T *p = base + (int64_t)min(grow, rows - 1) * ld + min(kk, kend - VEC);
+          const u32x4 x = *reinterpret_cast<const u32x4 *>(p);
+          v[i] = ok ? x : u32x4{0u, 0u, 0u, 0u};
         }
       }
     }
@@ -130,7 +134,6 @@ struct TrLoader {
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
           const int k = k0 + kb * VEC + j;
-          const T *p = base + (int64_t)k * ld + col;
           bool inside = true;
           if constexpr (KM) {
             int w = wpos + j, h = hpos;
@@ -142,10 +145,14 @@ struct TrLoader {
           }
           if constexpr (G) {
             const int valid = (k < kend && inside) ? (rows - col) : 0;
-            v[i][j] = load16<T>(p, valid, vec_ok);
+            v[i][j] = load16<T>(base + (int64_t)k * ld + col, valid, vec_ok);
           } else {
+            // fast path: rows % VEC == 0, so a chunk is whole or entirely out of range;
+            // out-of-range rows/columns load a clamped address and are zeroed
+            const bool ok = inside && k < kend && col < rows;
+            const T *p = base + (int64_t)min(k, kend - 1) * ld + min(col, rows - VEC);
             const u32x4 x = *reinterpret_cast<const u32x4 *>(p);
-            v[i][j] = inside ? x : u32x4{0u, 0u, 0u, 0u};
+            v[i][j] = ok ? x : u32x4{0u, 0u, 0u, 0u};
           }
         }
       }
@@ -210,6 +217,7 @@ struct KArgs {
   float *bias;
   float db_alpha, bias_lr;
   int cH, cW, cCi, cCo;  // 3x3 conv tile geometry (conv launches only)
+  int fast_ok;           // operand extents allow the clamped fast path (see the kernel)
 };
 
 // ------------------------------------------------------------------------- epilogue
@@ -385,8 +393,10 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
   constexpr int PASSES = BN / RPP;
   static_assert(NT % TPRW == 0 && BN % RPP == 0, "staged epilogue shape");
   const int er = tid / TPRW, ec = (tid % TPRW) * 4;
-  const bool full_tile = (m0 + BM <= g.M) && (n0 + BN <= g.N) && g.out_vec;
-  const bool sgd_fast = PREFETCH_W && full_tile && g.splits == 1 && g.epi.mode == EPI_SGD;
+  // Staged when the outputs allow 16-byte stores; ragged tiles guard each row and each
+  // group of 4 columns.
+  const bool staged = g.out_vec;
+  const bool sgd_fast = PREFETCH_W && staged && g.splits == 1 && g.epi.mode == EPI_SGD;
   f32x4 wold[PREFETCH_W ? PASSES : 1];
   if constexpr (PREFETCH_W) {
     if (sgd_fast) {
@@ -394,7 +404,10 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
 #pragma unroll
       for (int p = 0; p < PASSES; ++p) {
         const int n = n0 + p * RPP + er;
-        wold[p] = *reinterpret_cast<const f32x4 *>(w + (int64_t)n * g.epi.ldo + m0 + ec);
+        const int m = m0 + ec;
+        wold[p] = (n < g.N && m + 4 <= g.M)
+                      ? *reinterpret_cast<const f32x4 *>(w + (int64_t)n * g.epi.ldo + m)
+                      : f32x4{0.f, 0.f, 0.f, 0.f};
       }
     }
   }
@@ -420,8 +433,12 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
   // the main loop with plain vector loads and no branches around them, so the compiler's
   // wait counts cover exactly the tile being stored (the last iterations re-load the last
   // tile instead of skipping the load). Edge tiles run it with masked, conditional loads.
-  const bool interior = (m0 + BM <= g.M) && (n0 + BN <= g.N) && ((kend - kbeg) % BK == 0) &&
-                        g.a_vec && g.b_vec && nk > 0 && (nk % NSTAGE == 0);
+  // Fast path: aligned operands, whole 16-byte chunks (K ends and transposed-operand
+  // widths are multiples of VEC); ragged M/N/K edges are handled by clamped, zeroed loads
+  // and an odd tile count is padded with one all-zero tile.
+  const bool interior = g.a_vec && g.b_vec && nk > 0 && (kend % VEC == 0) &&
+                        (A_KC || g.M % VEC == 0) && (B_KC || g.N % VEC == 0) && g.fast_ok;
+  const int nk_fast = (nk + NSTAGE - 1) / NSTAGE * NSTAGE;
 
   auto compute = [&](int kt) {
     const char *sa = smem + (kt & 1) * STAGE;
@@ -497,8 +514,9 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
     constexpr bool G = decltype(gtag)::value;
     const int kg = kbeg + kt * BK;
     if constexpr (CONV == 2) {
-      // W[o][tap][c] read as A(c, o) for one tap
-      const int rs = kg / g.cCo, o0 = kg - rs * g.cCo;
+      // W[o][tap][c] read as A(c, o) for one tap; a tile past the K range reads nothing
+      const bool live = kg < kend;
+      const int rs = live ? kg / g.cCo : 0, o0 = live ? kg - rs * g.cCo : g.cCo;
       L.template load<G>(A + (int64_t)rs * g.cCi, g.lda, m0, g.M, o0, g.cCo, g.a_vec, tid);
     } else {
       L.template load<G>(A_rs, g.lda, m0, g.M, kg, kend, g.a_vec, tid);
@@ -509,11 +527,13 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
     const int kg = kbeg + kt * BK;
     if constexpr (CONV == 1) {
       // x_pad shifted by tap (r, s): B(c, P) = x_pad_flat[P + r*Wp + s][c]
-      const int rs = kg / g.cCi, c0 = kg - rs * g.cCi, r = rs / 3, sx = rs - 3 * r;
+      const bool live = kg < kend;
+      const int rs = live ? kg / g.cCi : 0, c0 = live ? kg - rs * g.cCi : g.cCi, r = rs / 3, sx = rs - 3 * r;
       L.template load<G>(Bp + (int64_t)(r * Wp + sx) * g.cCi, g.ldb, n0, g.N, c0, g.cCi, g.b_vec, tid_b);
     } else if constexpr (CONV == 2) {
       // dy_pad shifted by (2-r, 2-s): B(o, P) = dy_pad_flat[P + (2-r)*Wp + 2-s][o]
-      const int rs = kg / g.cCo, o0 = kg - rs * g.cCo, r = rs / 3, sx = rs - 3 * r;
+      const bool live = kg < kend;
+      const int rs = live ? kg / g.cCo : 0, o0 = live ? kg - rs * g.cCo : g.cCo, r = rs / 3, sx = rs - 3 * r;
       L.template load<G>(Bp + (int64_t)((2 - r) * Wp + 2 - sx) * g.cCo, g.ldb, n0, g.N, o0, g.cCo, g.b_vec,
                          tid_b);
     } else if constexpr (CONV == 3) {
@@ -527,7 +547,7 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
   const BoolTag<true> guarded{};
 
   if (interior) {
-    auto kc = [&](int kt) { return min(kt, nk - 1); };
+    auto kc = [&](int kt) { return kt; };
     issueA(la[0], 0, plain);
     issueB(lb[0], 0, plain);
     la[0].store(buf(0), tid);
@@ -537,7 +557,7 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
       issueB(lb[NSTAGE - 1], kc(1), plain);
     }
     __syncthreads();
-    for (int kt = 0; kt < nk; kt += NSTAGE) {
+    for (int kt = 0; kt < nk_fast; kt += NSTAGE) {
       if constexpr (NSTAGE == 2) {
         // step kt: set 1 holds tile kt+1; set 0 receives tile kt+2
         issueA(la[0], kc(kt + 2), plain);
@@ -599,7 +619,7 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
     }
   }
 
-  if (full_tile) {
+  if (staged) {
     // Stage the accumulator tile in LDS as [n][m] (pitch BM+4 floats), then let each group
     // of TPRW threads finish one whole row per pass.
     constexpr int PT = BM + 4;
@@ -616,6 +636,7 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
     for (int p = 0; p < PASSES; ++p) {
       const int nl = p * RPP + er;
       int n = n0 + nl;
+      if (n >= g.N || m >= g.M) continue;
       const f32x4 a = *reinterpret_cast<const f32x4 *>(stg + nl * PT + ec);
       if constexpr (CONV == 1 || CONV == 2) {
         n = conv_out_row(g, n);
@@ -626,7 +647,7 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
         continue;
       }
       if constexpr (PREFETCH_W) {
-        if (sgd_fast) {
+        if (sgd_fast && m + 4 <= g.M) {
           const Epilogue &e = g.epi;
           f32x4 nw;
 #pragma unroll
@@ -901,6 +922,7 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     g.mask_vec = e.mask && ((uintptr_t)e.mask % (4 * mes) == 0) && (e.ldmask % 4 == 0);
     g.bias_vec = e.bias && ((uintptr_t)e.bias % 16 == 0);
   }
+  g.fast_ok = 1;
   g.epi = p.epi;
   g.db_mode = p.db_mode;
   g.db_out = p.db_out;
@@ -1033,6 +1055,7 @@ static int conv_launch(int pass, int N, int H, int W, int Ci, int Co, const void
   g.tiles_n = cdiv(pl.N, pl.bn);
   g.a_vec = g.b_vec = 1;
   g.out_vec = 1;
+  g.fast_ok = 1;
   g.mask_vec = g.bias_vec = 0;
   g.epi = Epilogue{};
   g.epi.mode = EPI_STORE;
