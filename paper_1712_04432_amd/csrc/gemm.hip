@@ -691,6 +691,295 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
     }
 }
 
+// --------------------------------------------------- fused weight gradient + update
+// Delta_W = Delta_Y^T X (K = batch; both operands are stored with the batch as the row
+// index) with Eq. (1) applied in place: w -= lr*alpha*Delta_W, w16 = bf16(w), plus the
+// bias gradient (column sums of Delta_Y) on the tiles of the first column block. The
+// update streams 10 bytes per weight through HBM, so the kernel is built around that
+// stream. Persistent workgroups of eight waves in two groups:
+//  * waves 0-3 (MMA group) stream 32-row operand slabs of X and Delta_Y straight into a
+//    five-slot LDS ring with buffer loads that write LDS (no registers, four slabs in
+//    flight, out-of-range lanes read as zero), gather MFMA fragments with the LDS
+//    transpose read and accumulate the 128 x 128 tile in registers;
+//  * waves 4-7 (update group) finish the previous tile out of a separate LDS staging
+//    buffer: read-modify-write of the fp32 masters (prefetched one tile ahead), bf16 copy.
+// Each wave keeps its own memory counter, so the groups never wait on each other's
+// traffic; they meet at one barrier per slab and two per tile (staging free / full).
+constexpr int BUF_DW3 = 0x00020000;  // raw buffer resource word 3 (gfx9 family): 32-bit format
+
+struct DwArgs {
+  const uint16_t *X;   // [K][ldx]  rows are samples, M = d_in columns
+  const uint16_t *DY;  // [K][lddy] N = d_out columns
+  int64_t ldx, lddy;
+  int M, N, K;
+  float *w;            // [N][ldw] fp32 masters (read-modify-write)
+  int64_t ldw;
+  uint16_t *w16;       // [N][ldw16] bf16 copy
+  int64_t ldw16;
+  float lr, alpha;
+  int db_mode;         // 0 none, 1 store db_out, 2 bias -= bias_lr * db
+  float *db_out, *bias;
+  float db_alpha, bias_lr;
+  int tiles_m, tiles_n;
+};
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+__device__ __forceinline__ i32x4 buf_rsrc(const void *base) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = (int)(uint32_t)b;
+  r[1] = (int)((uint32_t)(b >> 32) & 0xffffu);  // stride 0
+  r[2] = 0x7fffffff;                             // bytes addressable through the descriptor
+  r[3] = BUF_DW3;
+  return r;
+}
+
+// One wave writes 64 x 16 bytes to LDS at lds_base + 16*lane from byte offsets voff of
+// the buffer; an offset at or past the descriptor's range writes zeros. Issued from
+// inline assembly so that the compiler does not drain the loads at every LDS read: the
+// caller waits for them explicitly (vmcnt) before the barrier that publishes the slab.
+// m0 (the LDS base of the write) is set inside the statement; on gfx9-family parts LDS
+// instructions do not read m0, and nothing else in the kernel that uses it relies on m0.
+__device__ __forceinline__ void dma16(const i32x4 &rsrc, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(lds_base)
+               : "memory");
+}
+
+template <int VM>
+__device__ __forceinline__ void vm_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(VM) : "memory");
+}
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory"); }
+
+__global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
+  constexpr int BM = 128, BN = 128, BK = 32, NS = 5, NTM = 256;
+  constexpr int ROWB = 256;                 // bytes per slab row: 128 bf16 columns
+  constexpr int PART = BK * ROWB;           // 8 KB per operand slab
+  constexpr int SLOT = 2 * PART;            // X slab then Delta_Y slab
+  constexpr int FM = 4, FN = 4;             // 16 x 16 fragments per wave (64 x 64)
+  constexpr int PT = BM + 4;                // staging pitch in floats
+  constexpr int RPP = NTM / (BM / 4), PASSES = BN / RPP;
+  constexpr int CHUNKS = 8, CP = PASSES / CHUNKS;
+  constexpr int DMA_PER_SLAB = 4;           // per wave: 2 x 1 KB of X, 2 x 1 KB of Delta_Y
+  constexpr uint32_t OOB = 0x80000000u;
+  __shared__ __attribute__((aligned(1024))) char smem[NS * SLOT + BN * PT * 4 + 4 * BN * 4];
+  float *stg = reinterpret_cast<float *>(smem + NS * SLOT);
+  float *dbred = stg + BN * PT;
+
+  const int tid = threadIdx.x;
+  const int tiles = a.tiles_m * a.tiles_n;
+  const int G = gridDim.x;
+  int b = blockIdx.x;
+  if ((G & 7) == 0) b = (b & 7) * (G >> 3) + (b >> 3);
+  const int nmy = b < tiles ? (tiles - 1 - b) / G + 1 : 0;
+  const int TK = (a.K + BK - 1) / BK;
+  auto tile_xy = [&](int it, int &m0, int &n0) {
+    const int t = b + it * G;
+    const int tm = t / a.tiles_n;
+    m0 = tm * BM;
+    n0 = (t - tm * a.tiles_n) * BN;
+  };
+
+  if (tid < NTM) {
+    // ------------------------------------------------------------------ MMA group
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm0 = (wave & 1) * 64, wn0 = (wave >> 1) * 64;
+    const i32x4 rx = buf_rsrc(a.X), rdy = buf_rsrc(a.DY);
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
+    // Slab layout: row r (sample k0 + r) holds 128 columns as 16 chunks of 16 bytes,
+    // chunk c stored at position c ^ swz(r), swz(r) = 2*(r & 3) + 8*((r >> 3) & 1): the
+    // 16 rows that one transpose read touches then cover every bank exactly twice.
+    // Loads: wave w fills rows 8w..8w+7 of both slabs, lane i row 8w + 4h + i/16 (h = 0, 1)
+    // and stored chunk i%16, which holds source chunk (i%16) ^ swz(row).
+    const int dr = lane >> 4, dc = lane & 15;
+    const int dsw = 2 * dr + 8 * (wave & 1);
+    const int dcol = 8 * (dc ^ dsw);              // source column within the tile
+    auto issue = [&](int s) {
+      // slab s of this workgroup's sequence: tile s / TK, rows (s % TK) * BK ...
+      const int it = s / TK;
+      const bool live = it < nmy;
+      int m0 = 0, n0 = 0;
+      if (live) tile_xy(it, m0, n0);
+      const int k0 = (s - it * TK) * BK;
+      const uint32_t slot = lds0 + (uint32_t)((s % NS) * SLOT);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = 8 * wave + 4 * h + dr;
+        const int k = k0 + r;
+        const bool kok = live && k < a.K;
+        const uint32_t ox = (kok && m0 + dcol < a.M) ? (uint32_t)(k * a.ldx + m0 + dcol) * 2u : OOB;
+        const uint32_t oy = (kok && n0 + dcol < a.N) ? (uint32_t)(k * a.lddy + n0 + dcol) * 2u : OOB;
+        const uint32_t dst = slot + (uint32_t)((8 * wave + 4 * h) * ROWB);
+        dma16(rx, ox, __builtin_amdgcn_readfirstlane(dst));
+        dma16(rdy, oy, __builtin_amdgcn_readfirstlane(dst + PART));
+      }
+    };
+    // Fragment reads: lane (kg = lane/16, s = lane%16) addresses row 8kg + s/4 (+4 for
+    // the second half of its 8 samples) at column c0 + 4*(s%4); the transpose read then
+    // hands lane s the 4 consecutive samples of column c0 + s.
+    const int kg = lane >> 4, fs = lane & 15;
+    const int fsw = 2 * (fs >> 2) + 8 * (kg & 1);
+    const uint32_t frow = (uint32_t)((8 * kg + (fs >> 2)) * ROWB + 8 * (fs & 1));
+    uint32_t fa_off[FM], fb_off[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa_off[i] = frow + (uint32_t)((((wm0 >> 3) + 2 * i + ((fs >> 1) & 1)) ^ fsw) * 16);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb_off[j] = PART + frow + (uint32_t)((((wn0 >> 3) + 2 * j + ((fs >> 1) & 1)) ^ fsw) * 16);
+    // Bias sums: thread t adds columns 4(t%32)..+3 over rows 4(t/32)..+3 of each slab.
+    const int bq = tid & 31, bk = tid >> 5;
+    const uint32_t db_off[4] = {
+        (uint32_t)(PART + (4 * bk + 0) * ROWB + (((bq >> 1) ^ (2 * ((4 * bk + 0) & 3) + 8 * (((4 * bk + 0) >> 3) & 1))) * 16) + 8 * (bq & 1)),
+        (uint32_t)(PART + (4 * bk + 1) * ROWB + (((bq >> 1) ^ (2 * ((4 * bk + 1) & 3) + 8 * (((4 * bk + 1) >> 3) & 1))) * 16) + 8 * (bq & 1)),
+        (uint32_t)(PART + (4 * bk + 2) * ROWB + (((bq >> 1) ^ (2 * ((4 * bk + 2) & 3) + 8 * (((4 * bk + 2) >> 3) & 1))) * 16) + 8 * (bq & 1)),
+        (uint32_t)(PART + (4 * bk + 3) * ROWB + (((bq >> 1) ^ (2 * ((4 * bk + 3) & 3) + 8 * (((4 * bk + 3) >> 3) & 1))) * 16) + 8 * (bq & 1))};
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float dbs[4] = {0.f, 0.f, 0.f, 0.f};
+
+    const int total = nmy * TK;
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) issue(s);
+    for (int s = 0; s < total; ++s) {
+      // Slab s landed once at most the later NS-2 slabs' loads are outstanding.
+      vm_barrier<(NS - 2) * DMA_PER_SLAB>();
+      issue(s + NS - 1);  // refills the slot read in the previous step
+      const int it = s / TK;
+      int m0, n0;
+      tile_xy(it, m0, n0);
+      const bool do_db = a.db_mode != 0 && m0 == 0;
+      const char *slot = smem + (s % NS) * SLOT;
+      i16x4 fa[FM][2], fb[FN][2];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        fa[i][0] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(slot + fa_off[i]));
+        fa[i][1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(slot + fa_off[i] + 4 * ROWB));
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        fb[j][0] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(slot + fb_off[j]));
+        fb[j][1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(slot + fb_off[j] + 4 * ROWB));
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const bf16x8 av = __builtin_bit_cast(bf16x8, __builtin_shufflevector(fa[i][0], fa[i][1], 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const bf16x8 bv = __builtin_bit_cast(bf16x8, __builtin_shufflevector(fb[j][0], fb[j][1], 0, 1, 2, 3, 4, 5, 6, 7));
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc[i][j], 0, 0, 0);
+        }
+      }
+      if (do_db) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const u32x2 q = *reinterpret_cast<const u32x2 *>(slot + db_off[r]);
+          dbs[0] += bf16_to_f32((uint16_t)(q[0] & 0xffffu));
+          dbs[1] += bf16_to_f32((uint16_t)(q[0] >> 16));
+          dbs[2] += bf16_to_f32((uint16_t)(q[1] & 0xffffu));
+          dbs[3] += bf16_to_f32((uint16_t)(q[1] >> 16));
+        }
+      }
+      if (s - it * TK == TK - 1) {
+        // tile done: hand the accumulator to the update group
+        if (do_db) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dbs[e] += __shfl_xor(dbs[e], 32, 64);
+          if (lane < 32) *reinterpret_cast<f32x4 *>(dbred + wave * BN + 4 * bq) = f32x4{dbs[0], dbs[1], dbs[2], dbs[3]};
+        }
+        lds_barrier();  // staging free (the update group is done with the previous tile)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) {
+            *reinterpret_cast<f32x4 *>(stg + (wn0 + j * 16 + fs) * PT + wm0 + i * 16 + kg * 4) = acc[i][j];
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        if (do_db) {
+          if (tid < BN) {
+            const float sum = dbred[tid] + dbred[BN + tid] + dbred[2 * BN + tid] + dbred[3 * BN + tid];
+            const int n = n0 + tid;
+            if (n < a.N) {
+              const float gb = a.db_alpha * sum;
+              if (a.db_mode == 1) a.db_out[n] = gb;
+              else a.bias[n] = fmaf(-a.bias_lr, gb, a.bias[n]);
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dbs[e] = 0.f;
+        }
+        lds_barrier();  // staging full
+      }
+    }
+    // Drain the ring's trailing loads (they target slots nobody reads again).
+    asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
+  } else {
+    // --------------------------------------------------------------- update group
+    // Branch-free buffer loads and stores on per-tile descriptors: a lane outside the
+    // matrix gets an offset past the descriptor's range, which the hardware drops
+    // (stores) or reads as zero (loads), so the compiler can count each master load
+    // exactly and never drains the store stream. Iteration it finishes tile it-1 (at
+    // it = 0 every store is dropped) while loading the masters of tile it, pass by pass,
+    // spread over the tile's slab barriers; the last iteration runs after the MMA group
+    // is done and passes no barrier.
+    const int et = tid - NTM;
+    const int er = et / (BM / 4), ec = (et % (BM / 4)) * 4;
+    f32x4 wold[PASSES];
+    int pm0 = 0, pn0 = a.N;
+    for (int it = 0; it <= nmy; ++it) {
+      const bool have = it < nmy;
+      int m0 = 0, n0 = a.N;
+      if (have) tile_xy(it, m0, n0);
+      const float *wn_base = have ? a.w + (int64_t)n0 * a.ldw + m0 : a.w;
+      float *wp_base = it > 0 ? a.w + (int64_t)pn0 * a.ldw + pm0 : a.w;
+      uint16_t *hp_base = it > 0 ? a.w16 + (int64_t)pn0 * a.ldw16 + pm0 : a.w16;
+      const __amdgpu_buffer_rsrc_t rn = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(wn_base), 0, 0x7fffffff, BUF_DW3);
+      const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(wp_base, 0, 0x7fffffff, BUF_DW3);
+      const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(hp_base, 0, 0x7fffffff, BUF_DW3);
+      const bool mp_ok = pm0 + ec < a.M, mn_ok = m0 + ec < a.M;
+#pragma unroll
+      for (int c = 0; c < CHUNKS; ++c) {
+#pragma unroll
+        for (int q = 0; q < CP; ++q) {
+          const int pp = c * CP + q;
+          const int nl = pp * RPP + er;
+          const bool vp = mp_ok && pn0 + nl < a.N;
+          const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + nl * PT + ec);
+          f32x4 nw;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) nw[e] = fmaf(-a.lr, a.alpha * v[e], wold[pp][e]);
+          u32x2 pk;
+          pk[0] = pack_bf16x2(nw[0], nw[1]);
+          pk[1] = pack_bf16x2(nw[2], nw[3]);
+          const uint32_t op = vp ? (uint32_t)(nl * a.ldw + ec) * 4u : OOB;
+          const uint32_t oh = vp ? (uint32_t)(nl * a.ldw16 + ec) * 2u : OOB;
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, nw), rp, op, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b64(pk, rh, oh, 0, 0);
+          const bool vn = mn_ok && n0 + nl < a.N;
+          const uint32_t on = vn ? (uint32_t)(nl * a.ldw + ec) * 4u : OOB;
+          wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rn, on, 0, 0));
+        }
+        if (have && c < TK) lds_barrier();
+      }
+      if (have) {
+        for (int c = CHUNKS; c < TK; ++c) lds_barrier();
+        lds_barrier();  // staging free
+        lds_barrier();  // staging full
+      }
+      pm0 = m0;
+      pn0 = n0;
+    }
+  }
+}
+
 // Sum the split partials in split order, then apply the epilogue.
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(KArgs g) {
   const int m4 = (g.M + 3) >> 2;
@@ -933,6 +1222,41 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   g.ldp = partial_ld(p.M);
   g.sstride = partial_split_stride(p.M, p.N);
 
+  // The fused update of a bf16 weight gradient runs on the dedicated persistent kernel.
+  if (p.dtype == IMBD_BF16 && !p.a_kc && !p.b_kc && p.epi.mode == EPI_SGD && pl.splits == 1 && g.out_vec &&
+      g.a_vec && g.b_vec && p.M % 8 == 0 && p.N % 8 == 0 && p.K % 8 == 0 && p.K > 0 && p.epi.out2 &&
+      !p.epi.mask && !p.epi.bias && !p.epi.relu && p.epi.ldo <= (1 << 22) && p.epi.ldo2 <= (1 << 22) &&
+      (int64_t)p.K * p.lda * 2 < (int64_t)1 << 31 && (int64_t)p.K * p.ldb * 2 < (int64_t)1 << 31 &&
+      env_int("IMBD_DW_GENERIC", 0) == 0) {
+    DwArgs d;
+    d.X = reinterpret_cast<const uint16_t *>(p.A);
+    d.DY = reinterpret_cast<const uint16_t *>(p.B);
+    d.ldx = p.lda;
+    d.lddy = p.ldb;
+    d.M = p.M;
+    d.N = p.N;
+    d.K = p.K;
+    d.w = reinterpret_cast<float *>(p.epi.out);
+    d.ldw = p.epi.ldo;
+    d.w16 = p.epi.out2;
+    d.ldw16 = p.epi.ldo2;
+    d.lr = p.epi.lr;
+    d.alpha = p.epi.alpha;
+    d.db_mode = p.db_mode;
+    d.db_out = p.db_out;
+    d.bias = p.bias;
+    d.db_alpha = p.db_alpha;
+    d.bias_lr = p.bias_lr;
+    d.tiles_m = cdiv(p.M, 128);
+    d.tiles_n = cdiv(p.N, 128);
+    const int tiles = d.tiles_m * d.tiles_n;
+    const int grid = tiles < 256 ? tiles : 256;
+    {
+      LaunchTimer t(p.kclass, p.layer, s);
+      hipLaunchKernelGGL(dw_sgd_kernel, dim3(grid), dim3(512), 0, s, d);
+    }
+    return check_launch("dw_sgd");
+  }
   const TileCfg &c = kCfgs[pl.cfg];
   KernelFn fn = c.fn[p.dtype == IMBD_BF16][p.a_kc][p.b_kc];
   const int grid = g.tiles_m * g.tiles_n * g.splits;

@@ -98,6 +98,28 @@ def test_bf16_one_step_matches_mirrored_oracle(imbd, dev, dims, B):
         assert nrm_err(host(layers[i]["db"]), ref["db"][i]) < TOL_BF16, i
 
 
+@pytest.mark.parametrize("dims,B", [((2056, 2104, 24), 72), ((136, 8, 16), 8), ((4096, 1000, 128), 256)])
+def test_bf16_fused_update_matches_oracle(imbd, dev, dims, B):
+    """The fused weight update (Eq. (1) applied inside the weight-gradient product) on
+    shapes that give the persistent update kernel several tiles per workgroup (17 x 17
+    tiles of the first layer), ragged tile edges and a batch that is not a multiple of
+    the 64-sample K tile; the bf16 copy must be the rounding of every new master."""
+    import torch
+    cfg = scaled_mlp(dims, B, "bf16")
+    _flush(f"bf16 fused update {dims} B={B}")
+    d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev, seed=11)
+    w0 = [host(l["w"]) for l in layers]
+    b0 = [host(l["b"]) for l in layers]
+    imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
+    torch.cuda.synchronize()
+    ref = oracle.train_step(w0, b0, xv, d["labels"], cfg.lr, "bf16")
+    for i in range(len(dims) - 1):
+        wn = host(layers[i]["w"])
+        assert nrm_err(wn - w0[i], ref["w"][i] - w0[i]) < TOL_BF16, i
+        assert nrm_err(host(layers[i]["b"]) - b0[i], ref["b"][i] - b0[i]) < TOL_BF16, i
+        assert np.array_equal(host(layers[i]["w_lp"]), oracle.round_bf16(wn)), i
+
+
 def test_bf16_ten_steps_match_mirrored_oracle(imbd, dev):
     """Ten fused steps on one fixed batch. Every step is compared with the oracle's step
     taken from the device's own state (masters and biases read back), at the bf16 bar,
