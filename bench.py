@@ -31,7 +31,7 @@ PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dw_sgd_alexnet_l1_traffic.txt")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_1712_04432_amd", "csrc", f) for f in ("gemm.hip", "common.h")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_1712_04432_amd", "csrc", f) for f in ("dw_sgd.hip", "cdna4.h", "common.h")]
 
 
 def log(msg):
@@ -183,6 +183,30 @@ def bench_conv(args):
     print(json.dumps(result), flush=True)
 
 
+def bench_copy(args):
+    """A plain device-to-device copy of 512 MiB: the calibration run for the HBM byte
+    counters (FETCH_SIZE / WRITE_SIZE per dispatch against the known 512 MiB each way)
+    and the practical copy bandwidth of the part."""
+    import torch
+    n = 512 << 20
+    a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    for _ in range(args.warmup):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        b.copy_(a)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    print(json.dumps({"metric": "device copy bandwidth (read + write)", "value": round(2 * n / (ms * 1e-3) / 1e9, 1),
+                      "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+                      "ms_per_step": round(ms, 5), "bytes_each_way": n}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -199,6 +223,8 @@ def main():
 
     if args.workload == "conv3x3_tile":
         return bench_conv(args)
+    if args.workload == "hbm_copy":
+        return bench_copy(args)
 
     import numpy as np
     import torch

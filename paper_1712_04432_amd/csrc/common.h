@@ -89,6 +89,10 @@ struct GemmPlan {
 };
 
 GemmPlan gemm_plan(const GemmProblem &p);
+// The persistent fused weight-gradient + update kernel (bf16, K <= 256): whether it
+// takes the problem, and the launch.
+bool dw_sgd_fits(const GemmProblem &p);
+int run_dw_sgd(const GemmProblem &p, hipStream_t s);
 // Enqueue the product; ws must hold plan.ws_bytes (partial sums) when splits > 1.
 int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s);
 

@@ -691,356 +691,6 @@ __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, 2)
     }
 }
 
-// --------------------------------------------------- fused weight gradient + update
-// Delta_W = Delta_Y^T X (K = batch; both operands are stored with the batch as the row
-// index) with Eq. (1) applied in place: w -= lr*alpha*Delta_W, w16 = bf16(w), plus the
-// bias gradient (column sums of Delta_Y) on the tiles of the first column block. The
-// update streams 10 bytes per weight through HBM, so the kernel is built around that
-// stream. Persistent workgroups of eight waves in two groups:
-//  * waves 0-3 (MMA group) stream 32-row operand slabs of X and Delta_Y straight into a
-//    five-slot LDS ring with buffer loads that write LDS (no registers, four slabs in
-//    flight, out-of-range lanes read as zero), gather MFMA fragments with the LDS
-//    transpose read and accumulate the 128 x 128 tile in registers;
-//  * waves 4-7 (update group) finish the previous tile out of a separate LDS staging
-//    buffer: read-modify-write of the fp32 masters (prefetched one tile ahead), bf16 copy.
-// Each wave keeps its own memory counter, so the groups never wait on each other's
-// traffic; they meet at one barrier per slab and two per tile (staging free / full).
-constexpr int BUF_DW3 = 0x00020000;  // raw buffer resource word 3 (gfx9 family): 32-bit format
-// Cache-policy operand of the master loads and stores: default policy. (The
-// non-temporal bit cut the L2 misses of the operand loads but slowed the master stream
-// itself by more on most layer shapes.)
-constexpr int CPOL_MASTER = 0;
-
-struct DwArgs {
-  const uint16_t *X;   // [K][ldx]  rows are samples, M = d_in columns
-  const uint16_t *DY;  // [K][lddy] N = d_out columns
-  int64_t ldx, lddy;
-  int M, N, K;
-  float *w;            // [N][ldw] fp32 masters (read-modify-write)
-  int64_t ldw;
-  uint16_t *w16;       // [N][ldw16] bf16 copy
-  int64_t ldw16;
-  float lr, alpha;
-  int db_mode;         // 0 none, 1 store db_out, 2 bias -= bias_lr * db
-  float *db_out, *bias;
-  float db_alpha, bias_lr;
-  int tiles_m, tiles_n;
-};
-
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-
-__device__ __forceinline__ i32x4 buf_rsrc(const void *base, uint32_t bytes) {
-  const uint64_t b = reinterpret_cast<uint64_t>(base);
-  i32x4 r;
-  r[0] = (int)(uint32_t)b;
-  r[1] = (int)((uint32_t)(b >> 32) & 0xffffu);  // stride 0
-  r[2] = (int)bytes;                             // offsets at or past this read as zero
-  r[3] = BUF_DW3;
-  return r;
-}
-
-// One wave writes 64 x 16 bytes to LDS at lds_base + 16*lane from byte offsets voff of
-// the buffer; an offset at or past the descriptor's range writes zeros. Issued from
-// inline assembly so that the compiler does not drain the loads at every LDS read: the
-// caller waits for them explicitly (vmcnt) before the barrier that publishes the slab.
-// m0 (the LDS base of the write) is set inside the statement; on gfx9-family parts LDS
-// instructions do not read m0, and nothing else in the kernel that uses it relies on m0.
-__device__ __forceinline__ void dma16(const i32x4 &rsrc, uint32_t voff, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-               :
-               : "v"(voff), "s"(rsrc), "s"(lds_base)
-               : "memory");
-}
-
-template <int VM>
-__device__ __forceinline__ void vm_barrier() {
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(VM) : "memory");
-}
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory"); }
-
-// Two floats to packed bf16, round to nearest even (the gfx950 conversion instruction).
-__device__ __forceinline__ uint32_t cvt_pk_bf16(float x, float y) {
-  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-  typedef float f32x2_t __attribute__((ext_vector_type(2)));
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){x, y}, bf16x2_t));
-}
-
-__global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
-  constexpr int BM = 128, BN = 128, BK = 32, NS = 4, NTM = 256, NTU = 256, KMAX = 256;
-  constexpr int ROWB = 256;                 // bytes per LDS row: 128 bf16 columns
-  constexpr int XSLAB = BK * ROWB;          // 8 KB X slab
-  constexpr int DYB = KMAX * ROWB;          // 64 KB resident Delta_Y column block
-  constexpr int FM = 4, FN = 4;             // 16 x 16 fragments per wave (64 x 64)
-  constexpr int RPP = NTU / (BM / 4), PASSES = BN / RPP;
-  constexpr int CHUNKS = 8, CP = PASSES / CHUNKS;
-  constexpr int DMA_PER_SLAB = 2;           // per wave: 2 x 1 KB of X
-  constexpr uint32_t OOB = 0x80000000u;
-  // [X ring][resident Delta_Y block][staging, 128 x 128 fp32 with 16-byte units swizzled]
-  __shared__ __attribute__((aligned(1024))) char smem[NS * XSLAB + DYB + BN * BM * 4];
-  char *dyres = smem + NS * XSLAB;
-  float *stg = reinterpret_cast<float *>(dyres + DYB);
-
-  const int tid = threadIdx.x;
-  const int tiles = a.tiles_m * a.tiles_n;
-  const int G = gridDim.x;  // a multiple of tiles_n: every tile of a workgroup has the same column block
-  int b = blockIdx.x;
-  if ((G & 7) == 0) b = (b & 7) * (G >> 3) + (b >> 3);
-  const int nmy = b < tiles ? (tiles - 1 - b) / G + 1 : 0;
-  const int TK = (a.K + BK - 1) / BK;
-  const int n0 = (b % a.tiles_n) * BN;
-  auto tile_m0 = [&](int it) { return ((b + it * G) / a.tiles_n) * BM; };
-
-  if (tid < NTM) {
-    // ------------------------------------------------------------------ MMA group
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm0 = (wave & 1) * 64, wn0 = (wave >> 1) * 64;
-    // Rows past the batch fall outside the descriptors' ranges and read as zero.
-    const i32x4 rx = buf_rsrc(a.X, (uint32_t)(a.K * a.ldx * 2));
-    const i32x4 rdy = buf_rsrc(a.DY, (uint32_t)(a.K * a.lddy * 2));
-    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
-    const uint32_t ldy = lds0 + NS * XSLAB;
-    // LDS row layout (X slabs and the Delta_Y block alike): row r (sample r of the slab or
-    // block) holds 128 columns as 16 chunks of 16 bytes, chunk c stored at position
-    // c ^ swz(r), swz(r) = 2*(r & 3) + 8*((r >> 3) & 1): the 16 rows that one transpose
-    // read touches then cover every bank exactly twice. A wave's 1 KB load covers 4 rows:
-    // lane i fills row 4q + i/16, stored chunk i%16, from source chunk (i%16) ^ swz(row).
-    const int dr = lane >> 4, dc = lane & 15;
-    // resident Delta_Y block: wave w loads rows 64w..64w+63, 16 loads of 4 rows
-    {
-#pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int r = 64 * wave + 4 * q + dr;
-        const int scol = 8 * (dc ^ (2 * dr + 8 * ((q >> 1) & 1)));  // source column of the lane's chunk
-        const uint32_t off = n0 + scol < a.N ? (uint32_t)((r * a.lddy + n0 + scol) * 2) : OOB;
-        dma16(rdy, off, __builtin_amdgcn_readfirstlane(ldy + (uint32_t)((64 * wave + 4 * q) * ROWB)));
-      }
-    }
-    // X slabs: wave w fills rows 8w..8w+7 of each slab (two 4-row loads)
-    const int dcol = 8 * (dc ^ (2 * dr + 8 * (wave & 1)));
-    const uint32_t xstep = (uint32_t)(BK * a.ldx * 2), xh = (uint32_t)(4 * a.ldx * 2);
-    int i_it = 0, i_ks = 0;
-    uint32_t i_slot = 0, xk = 0, xb = OOB;
-    auto i_tile = [&]() {
-      xb = OOB;
-      if (i_it < nmy) {
-        const int m0 = tile_m0(i_it);
-        if (m0 + dcol < a.M) xb = (uint32_t)(((8 * wave + dr) * a.ldx + m0 + dcol) * 2);
-      }
-      xk = 0;
-    };
-    auto issue = [&]() {
-      const uint32_t dst = lds0 + i_slot + (uint32_t)(8 * wave * ROWB);
-      dma16(rx, xb + xk, dst);
-      dma16(rx, xb + xh + xk, dst + 4 * ROWB);
-      i_slot = i_slot + XSLAB == NS * XSLAB ? 0u : i_slot + XSLAB;
-      xk += xstep;
-      if (++i_ks == TK) {
-        i_ks = 0;
-        ++i_it;
-        i_tile();
-      }
-    };
-
-    // Fragment reads: lane (kg = lane/16, s = lane%16) addresses row 8kg + s/4 (+4 for
-    // the second half of its 8 samples) at column c0 + 4*(s%4); the transpose read then
-    // hands lane s the 4 consecutive samples of column c0 + s.
-    const int kg = lane >> 4, fs = lane & 15;
-    const int fsw = 2 * (fs >> 2) + 8 * (kg & 1);
-    const uint32_t frow = (uint32_t)((8 * kg + (fs >> 2)) * ROWB + 8 * (fs & 1));
-    uint32_t fa_off[FM], fb_off[FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i) fa_off[i] = lds0 + frow + (uint32_t)((((wm0 >> 3) + 2 * i + ((fs >> 1) & 1)) ^ fsw) * 16);
-#pragma unroll
-    for (int j = 0; j < FN; ++j) fb_off[j] = ldy + frow + (uint32_t)((((wn0 >> 3) + 2 * j + ((fs >> 1) & 1)) ^ fsw) * 16);
-
-    f32x4 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    auto read_slab = [&](uint32_t slot, uint32_t krow, i16x4 (&xa)[FM][2], i16x4 (&xb2)[FN][2]) {
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        lds_i16x4 *p = (lds_i16x4 *)(uintptr_t)(fa_off[i] + slot);
-        xa[i][0] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p);
-        xa[i][1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p + 4 * ROWB / 8);
-      }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        lds_i16x4 *p = (lds_i16x4 *)(uintptr_t)(fb_off[j] + krow);
-        xb2[j][0] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p);
-        xb2[j][1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p + 4 * ROWB / 8);
-      }
-    };
-    auto mma = [&](const i16x4 (&xa)[FM][2], const i16x4 (&xb2)[FN][2]) {
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const bf16x8 av = __builtin_bit_cast(bf16x8, __builtin_shufflevector(xa[i][0], xa[i][1], 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const bf16x8 bv = __builtin_bit_cast(bf16x8, __builtin_shufflevector(xb2[j][0], xb2[j][1], 0, 1, 2, 3, 4, 5, 6, 7));
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc[i][j], 0, 0, 0);
-        }
-      }
-    };
-    // Staging layout: element (n, m) at float n*128 + 4*((m/4) ^ (n % 32)) + m%4.
-    auto handoff = [&]() {
-      lds_barrier();  // staging free (the update group is done with the previous tile)
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int n = wn0 + j * 16 + fs, m4 = (wm0 >> 2) + i * 4 + kg;
-          *reinterpret_cast<f32x4 *>(stg + n * BM + 4 * (m4 ^ (n & 31))) = acc[i][j];
-          acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-      lds_barrier();  // staging full
-    };
-
-    const int total = nmy * TK;
-    i_tile();
-#pragma unroll
-    for (int s = 0; s < NS; ++s) issue();
-    vm_barrier<(NS - 1) * DMA_PER_SLAB>();  // Delta_Y block and slab 0 landed
-
-    // Bias gradient: the column sums of Delta_Y, once, by the workgroups whose first tile
-    // is in the first row block. Lanes l and l+32 of a wave split the batch of one column.
-    if (a.db_mode != 0 && b < a.tiles_n && nmy > 0) {
-      const int c = wave * 32 + (lane & 31), half = lane >> 5;
-      const int kh = (KMAX / 2);
-      float sum = 0.f;
-      for (int r = half * kh; r < half * kh + kh; ++r) {
-        const int sw = 2 * (r & 3) + 8 * ((r >> 3) & 1);
-        const uint16_t v = *(const __attribute__((address_space(3))) uint16_t *)(uintptr_t)(
-            ldy + (uint32_t)(r * ROWB + (((c >> 3) ^ sw) << 4) + 2 * (c & 7)));
-        sum += bf16_to_f32(v);
-      }
-      sum += __shfl_xor(sum, 32, 64);
-      const int n = n0 + c;
-      if (half == 0 && n < a.N) {
-        const float g = a.db_alpha * sum;
-        if (a.db_mode == 1) a.db_out[n] = g;
-        else a.bias[n] = fmaf(-a.bias_lr, g, a.bias[n]);
-      }
-    }
-
-    int c_ks = 0;
-    uint32_t c_slot = 0, c_krow = 0;
-    i16x4 fa[FM][2], fb[FN][2], ga[FM][2], gb[FN][2];
-    read_slab(c_slot, c_krow, fa, fb);
-    auto step = [&](const i16x4 (&ca)[FM][2], const i16x4 (&cb)[FN][2], i16x4 (&na)[FM][2], i16x4 (&nb)[FN][2]) {
-      // Slab s+1 landed once at most the later NS-2 slabs' loads are outstanding; every
-      // wave has read slab s, so its slot takes the next slab in line.
-      vm_barrier<(NS - 2) * DMA_PER_SLAB>();
-      issue();
-      c_slot = c_slot + XSLAB == NS * XSLAB ? 0u : c_slot + XSLAB;
-      const bool tile_end = ++c_ks == TK;
-      c_krow += BK * ROWB;
-      if (tile_end) {
-        c_ks = 0;
-        c_krow = 0;
-      }
-      // The MFMAs of slab s go first: the transpose reads of slab s+1 then run while
-      // the matrix pipe works, with no wait between them.
-      mma(ca, cb);
-      __builtin_amdgcn_sched_barrier(0);
-      read_slab(c_slot, c_krow, na, nb);
-      if (tile_end) handoff();
-    };
-    // Two steps per trip so that the fragment sets alternate without copies.
-    for (int s = 0; s < total; s += 2) {
-      step(fa, fb, ga, gb);
-      if (s + 1 >= total) break;
-      step(ga, gb, fa, fb);
-    }
-    // Drain the ring's trailing loads (they target slots nobody reads again).
-    asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
-  } else {
-    // --------------------------------------------------------------- update group
-    // Branch-free buffer loads and stores on per-tile descriptors. Rows past the matrix
-    // fall outside the descriptor's range and a lane whose columns are past it gets an
-    // out-of-range base, so the hardware drops those stores and reads those loads as
-    // zero; with no conditional memory operation the compiler counts each master load
-    // exactly and never drains the store stream. Iteration it finishes tile it-1 (at
-    // it = 0 every store is dropped: empty range) while loading the masters of tile it,
-    // pass by pass, spread over the tile's slab barriers; the last iteration runs after
-    // the MMA group is done and passes no barrier.
-    const int et = tid - NTM;
-    const int er = et / (BM / 4), ec = (et % (BM / 4)) * 4;
-    const float c = -a.lr * a.alpha;
-    const uint32_t wrow = (uint32_t)(RPP * a.ldw * 4), hrow = (uint32_t)(RPP * a.ldw16 * 2);
-    // staging row pp*RPP + er, 16-byte unit (ec/4) ^ ((pp*RPP + er) % 32): four lane bases
-    uint32_t sb[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      sb[q] = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)stg + (uint32_t)(er * BM * 4 + (((ec >> 2) ^ (er + 8 * q)) << 4));
-    const int nrows = min(BN, a.N - n0);
-    // A master vector is loaded CHUNKS - LAG chunks (slab barriers) before the pass that
-    // needs it: far enough ahead to cover the HBM latency, near enough that the CU's queue
-    // of outstanding requests stays short and the operand loads are not stuck behind it.
-    constexpr int LAG = 4;
-    f32x4 wold[PASSES];
-    int pm0 = 0;
-    lds_barrier();  // matches the MMA group's "Delta_Y block and slab 0 landed"
-    for (int it = 0; it <= nmy; ++it) {
-      const bool have = it < nmy;
-      const int m0 = have ? tile_m0(it) : 0;
-      // rn: tile it (masters for passes loaded late in this iteration), rq: tile it-1
-      // (loaded early in this iteration), rp/rh: tile it-1 (finished in this iteration)
-      const float *wn_base = a.w + (int64_t)n0 * a.ldw + m0;
-      const float *wq_base = a.w + (int64_t)n0 * a.ldw + pm0;
-      float *wp_base = a.w + (int64_t)n0 * a.ldw + pm0;
-      uint16_t *hp_base = a.w16 + (int64_t)n0 * a.ldw16 + pm0;
-      const int rn_rows = have ? nrows : 0, rp_rows = it > 0 ? nrows : 0;
-      const __amdgpu_buffer_rsrc_t rn = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(wn_base), 0, rn_rows * (int)a.ldw * 4, BUF_DW3);
-      const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(wq_base), 0, rp_rows * (int)a.ldw * 4, BUF_DW3);
-      const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(wp_base, 0, rp_rows * (int)a.ldw * 4, BUF_DW3);
-      const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(hp_base, 0, rp_rows * (int)a.ldw16 * 2, BUF_DW3);
-      const uint32_t vp = pm0 + ec < a.M ? (uint32_t)(er * a.ldw + ec) * 4u : OOB;
-      const uint32_t vh = pm0 + ec < a.M ? (uint32_t)(er * a.ldw16 + ec) * 2u : OOB;
-      const uint32_t vn = m0 + ec < a.M ? (uint32_t)(er * a.ldw + ec) * 4u : OOB;
-#pragma unroll
-      for (int ch = 0; ch < CHUNKS; ++ch) {
-#pragma unroll
-        for (int q = 0; q < CP; ++q) {
-          const int pp = ch * CP + q;
-          const f32x4 v = *(const __attribute__((address_space(3))) f32x4 *)(uintptr_t)(sb[pp & 3] + pp * RPP * BM * 4);
-          f32x4 nw;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) nw[e] = fmaf(c, v[e], wold[pp][e]);
-          u32x2 pk;
-          pk[0] = cvt_pk_bf16(nw[0], nw[1]);
-          pk[1] = cvt_pk_bf16(nw[2], nw[3]);
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, nw), rp, vp + pp * wrow, 0, CPOL_MASTER);
-          __builtin_amdgcn_raw_buffer_store_b64(pk, rh, vh + pp * hrow, 0, CPOL_MASTER);
-        }
-        // refill the registers of chunk ch - LAG (tile it) or ch - LAG + CHUNKS (tile it-1)
-#pragma unroll
-        for (int q = 0; q < CP; ++q) {
-          if (ch >= LAG) {
-            const int pp = (ch - LAG) * CP + q;
-            wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rn, vn + pp * wrow, 0, CPOL_MASTER));
-          } else {
-            const int pp = (ch - LAG + CHUNKS) * CP + q;
-            wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, vp + pp * wrow, 0, CPOL_MASTER));
-          }
-        }
-        if (have && ch < TK) lds_barrier();
-      }
-      if (have) {
-        for (int ch = CHUNKS; ch < TK; ++ch) lds_barrier();
-        lds_barrier();  // staging free
-        lds_barrier();  // staging full
-      }
-      pm0 = m0;
-    }
-  }
-}
-
 // Sum the split partials in split order, then apply the epilogue.
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(KArgs g) {
   const int m4 = (g.M + 3) >> 2;
@@ -1283,43 +933,8 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   g.ldp = partial_ld(p.M);
   g.sstride = partial_split_stride(p.M, p.N);
 
-  // The fused update of a bf16 weight gradient runs on the dedicated persistent kernel.
-  if (p.dtype == IMBD_BF16 && !p.a_kc && !p.b_kc && p.epi.mode == EPI_SGD && pl.splits == 1 && g.out_vec &&
-      g.a_vec && g.b_vec && p.M % 8 == 0 && p.N % 8 == 0 && p.K % 8 == 0 && p.K > 0 && p.K <= 256 && p.N <= 256 * 128 && p.epi.out2 &&
-      !p.epi.mask && !p.epi.bias && !p.epi.relu && p.epi.ldo < (1 << 21) && p.epi.ldo2 < (1 << 21) &&
-      (int64_t)p.K * p.lda * 2 < (int64_t)1 << 31 && (int64_t)p.K * p.ldb * 2 < (int64_t)1 << 31 &&
-      env_int("IMBD_DW_GENERIC", 0) == 0) {
-    DwArgs d;
-    d.X = reinterpret_cast<const uint16_t *>(p.A);
-    d.DY = reinterpret_cast<const uint16_t *>(p.B);
-    d.ldx = p.lda;
-    d.lddy = p.ldb;
-    d.M = p.M;
-    d.N = p.N;
-    d.K = p.K;
-    d.w = reinterpret_cast<float *>(p.epi.out);
-    d.ldw = p.epi.ldo;
-    d.w16 = p.epi.out2;
-    d.ldw16 = p.epi.ldo2;
-    d.lr = p.epi.lr;
-    d.alpha = p.epi.alpha;
-    d.db_mode = p.db_mode;
-    d.db_out = p.db_out;
-    d.bias = p.bias;
-    d.db_alpha = p.db_alpha;
-    d.bias_lr = p.bias_lr;
-    d.tiles_m = cdiv(p.M, 128);
-    d.tiles_n = cdiv(p.N, 128);
-    // One workgroup per CU at most, and a multiple of the column-block count so that a
-    // workgroup's tiles share one Delta_Y column block (kept in LDS).
-    const int tiles = d.tiles_m * d.tiles_n;
-    const int grid = tiles < 256 ? tiles : (256 / d.tiles_n) * d.tiles_n;
-    {
-      LaunchTimer t(p.kclass, p.layer, s);
-      hipLaunchKernelGGL(dw_sgd_kernel, dim3(grid), dim3(512), 0, s, d);
-    }
-    return check_launch("dw_sgd");
-  }
+  // The fused update of a bf16 weight gradient runs on its own persistent kernel.
+  if (dw_sgd_fits(p) && env_int("IMBD_DW_GENERIC", 0) == 0) return run_dw_sgd(p, s);
   const TileCfg &c = kCfgs[pl.cfg];
   KernelFn fn = c.fn[p.dtype == IMBD_BF16][p.a_kc][p.b_kc];
   const int grid = g.tiles_m * g.tiles_n * g.splits;

@@ -22,8 +22,11 @@ def short_name(name: str) -> str:
     return name.replace("imbd::", "").replace("unsigned short", "bf16")
 
 
-def summarize(path: str):
-    rows = list(csv.DictReader(open(path)))
+def summarize(path: str, per_step_ref: str = ""):
+    """Group launches by (kernel, grid, workgroup size). With per_step_ref (a kernel that
+    runs once per step), a group with n launches per step is split further by the
+    launch's position within the step, so that e.g. the layers of one kernel separate."""
+    rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Start_Timestamp"]))
     groups = collections.defaultdict(list)
     for r in rows:
         wg = int(r["Workgroup_Size_X"]) * int(r.get("Workgroup_Size_Y", 1) or 1) * int(r.get("Workgroup_Size_Z", 1) or 1)
@@ -31,6 +34,14 @@ def summarize(path: str):
         grid = items // max(wg, 1)
         dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0
         groups[(short_name(r["Kernel_Name"]), grid, wg)].append(dur)
+    if per_step_ref:
+        steps = sum(len(v) for k, v in groups.items() if per_step_ref in k[0])
+        split = collections.defaultdict(list)
+        for (name, grid, wg), v in groups.items():
+            per = len(v) // steps if steps and len(v) % steps == 0 and len(v) >= steps else 1
+            for i, d in enumerate(v):
+                split[(name if per == 1 else f"{name} [{i % per + 1}/{per}]", grid, wg)].append(d)
+        groups = split
     total = sum(sum(v) for v in groups.values())
     out = []
     for (name, grid, wg), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
@@ -40,13 +51,37 @@ def summarize(path: str):
     return out
 
 
+def counter_per_dispatch(path: str, kernel: str, counter: str):
+    """Per-dispatch totals of one counter (summed over the instances rocprofv3 reports)
+    for the dispatches whose kernel name contains `kernel`, in dispatch order."""
+    tot = collections.OrderedDict()
+    for r in csv.DictReader(open(path)):
+        if kernel in r["Kernel_Name"] and r["Counter_Name"] == counter:
+            d = int(r["Dispatch_Id"])
+            tot[d] = tot.get(d, 0.0) + float(r["Counter_Value"])
+    return [tot[d] for d in sorted(tot)]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("trace")
     ap.add_argument("--title", default="")
     ap.add_argument("--top", type=int, default=30)
+    ap.add_argument("--counter", default="", help="summarise this counter of a --pmc run instead")
+    ap.add_argument("--kernel", default="", help="kernel-name substring for --counter")
+    ap.add_argument("--per-step-ref", default="", help="kernel launched once per step (splits layers)")
+    ap.add_argument("--period", type=int, default=1,
+                    help="dispatches of the kernel per step; one median per position in the step")
     a = ap.parse_args()
-    rows = summarize(a.trace)
+    if a.counter:
+        v = counter_per_dispatch(a.trace, a.kernel, a.counter)
+        print(f"{a.counter} per dispatch of '{a.kernel}' ({len(v)} dispatches)")
+        for k in range(a.period):
+            s = v[k::a.period]
+            if s:
+                print(f"  position {k}: median {statistics.median(s):.1f}  min {min(s):.1f}  max {max(s):.1f}  (n={len(s)})")
+        return
+    rows = summarize(a.trace, a.per_step_ref)
     if a.title:
         print(a.title)
         print()
