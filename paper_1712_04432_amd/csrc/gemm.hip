@@ -837,13 +837,20 @@ inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 // Split-K partial sums: [split][n][ldp] fp32. Row pitch and split pitch are kept off powers
 // of two (+256 B and +4.25 KiB) so the splits of one output do not all map to the same
 // DRAM bank.
-inline int64_t partial_ld(int M) { return ((int64_t)M + 7) / 8 * 8 + 64; }
-inline int64_t partial_split_stride(int M, int N) { return (int64_t)N * partial_ld(M) + 1088; }
 
 }  // namespace
 
 GemmPlan gemm_plan(const GemmProblem &p) {
   GemmPlan pl{};
+  if (skinny_fits(p) && env_int("IMBD_SKINNY_OFF", 0) == 0) {
+    // the skinny-batch product always goes through fp32 partials (one per K split)
+    skinny_plan(p, &pl.splits, &pl.k_split);
+    pl.cfg = -1;
+    pl.bm = 64;
+    pl.bn = 256;
+    pl.ws_bytes = (size_t)pl.splits * (size_t)partial_split_stride(p.M, p.N) * sizeof(float);
+    return pl;
+  }
   const int esz = p.dtype == IMBD_BF16 ? 2 : 4;
   const int BK = KT_BYTES / esz;
   // Tile: the largest configuration that still gives a reasonable number of tiles.
@@ -877,6 +884,35 @@ GemmPlan gemm_plan(const GemmProblem &p) {
   return pl;
 }
 
+// Adds the split partials in split order and applies the epilogue.
+static int launch_reduce(const GemmProblem &p, const KArgs &g, hipStream_t s) {
+  // the lean kernel needs 8-aligned rows (M, ld and pointers) and a store epilogue
+  const Epilogue &e = p.epi;
+  const int oes = e.out_dtype == IMBD_BF16 ? 2 : 4;
+  const bool lean = e.mode == EPI_STORE && p.M % 8 == 0 && e.ldo % 8 == 0 && (uintptr_t)e.out % (8 * oes) == 0 &&
+                    (!e.bias || (uintptr_t)e.bias % 32 == 0) &&
+                    (!e.mask || (e.ldmask % 8 == 0 && (uintptr_t)e.mask % (e.mask_dtype == IMBD_BF16 ? 16 : 32) == 0)) &&
+                    g.ldp % 8 == 0 && g.sstride % 8 == 0 && p.N <= 65535;
+  LaunchTimer t(IMBD_K_SPLITK, p.layer, s);
+  if (lean) {
+    const dim3 grid((unsigned)((p.M / 8 + 255) / 256), (unsigned)p.N);
+    const bool bf = e.out_dtype == IMBD_BF16;
+    if (e.mask) {
+      if (bf) hipLaunchKernelGGL((splitk_reduce_fast<true, true>), grid, dim3(256), 0, s, g);
+      else hipLaunchKernelGGL((splitk_reduce_fast<false, true>), grid, dim3(256), 0, s, g);
+    } else {
+      if (bf) hipLaunchKernelGGL((splitk_reduce_fast<true, false>), grid, dim3(256), 0, s, g);
+      else hipLaunchKernelGGL((splitk_reduce_fast<false, false>), grid, dim3(256), 0, s, g);
+    }
+  } else {
+    const int64_t total = (int64_t)p.N * ((p.M + 3) / 4);
+    int blocks = (int)((total + 255) / 256);
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, g);
+  }
+  return check_launch("splitk_reduce");
+}
+
 int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   if (p.db_mode != 0 && p.b_kc) {
     set_error("bias sums need the B operand stored [k][n]");
@@ -884,15 +920,16 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   }
   if (p.M <= 0 || p.N <= 0) return IMBD_OK;
   const GemmPlan pl = gemm_plan(p);
-  if (pl.splits > 1 && (ws == nullptr || ws_bytes < pl.ws_bytes)) {
+  if (pl.ws_bytes > 0 && (ws == nullptr || ws_bytes < pl.ws_bytes)) {
     set_error("product %dx%dx%d needs %zu bytes of workspace for split-K partials, got %zu",
               p.M, p.N, p.K, pl.ws_bytes, ws_bytes);
     return IMBD_EWORKSPACE;
   }
-  if (pl.splits > 1 && (uintptr_t)ws % 16 != 0) {
+  if (pl.ws_bytes > 0 && (uintptr_t)ws % 16 != 0) {
     set_error("workspace must be 16-byte aligned");
     return IMBD_EINVAL;
   }
+  if (pl.cfg < 0) return run_skinny(p, ws, s);
   const int esz = p.dtype == IMBD_BF16 ? 2 : 4;
   KArgs g;
   g.A = p.A;
@@ -950,34 +987,27 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
                        p.db_mode == 2 ? p.bias : nullptr, p.bias_lr, s, p.layer);
     if (rc != IMBD_OK) return rc;
   }
-  if (pl.splits > 1) {
-    // the lean kernel needs 8-aligned rows (M, ld and pointers) and a store epilogue
-    const Epilogue &e = p.epi;
-    const int oes = e.out_dtype == IMBD_BF16 ? 2 : 4;
-    const bool lean = e.mode == EPI_STORE && p.M % 8 == 0 && e.ldo % 8 == 0 && (uintptr_t)e.out % (8 * oes) == 0 &&
-                      (!e.bias || (uintptr_t)e.bias % 32 == 0) &&
-                      (!e.mask || (e.ldmask % 8 == 0 && (uintptr_t)e.mask % (e.mask_dtype == IMBD_BF16 ? 16 : 32) == 0)) &&
-                      g.ldp % 8 == 0 && g.sstride % 8 == 0 && p.N <= 65535;
-    LaunchTimer t(IMBD_K_SPLITK, p.layer, s);
-    if (lean) {
-      const dim3 grid((unsigned)((p.M / 8 + 255) / 256), (unsigned)p.N);
-      const bool bf = e.out_dtype == IMBD_BF16;
-      if (e.mask) {
-        if (bf) hipLaunchKernelGGL((splitk_reduce_fast<true, true>), grid, dim3(256), 0, s, g);
-        else hipLaunchKernelGGL((splitk_reduce_fast<false, true>), grid, dim3(256), 0, s, g);
-      } else {
-        if (bf) hipLaunchKernelGGL((splitk_reduce_fast<true, false>), grid, dim3(256), 0, s, g);
-        else hipLaunchKernelGGL((splitk_reduce_fast<false, false>), grid, dim3(256), 0, s, g);
-      }
-    } else {
-      const int64_t total = (int64_t)p.N * ((p.M + 3) / 4);
-      int blocks = (int)((total + 255) / 256);
-      if (blocks > 4096) blocks = 4096;
-      hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, g);
-    }
-    rc = check_launch("splitk_reduce");
-  }
+  if (pl.splits > 1) rc = launch_reduce(p, g, s);
   return rc;
+}
+
+int run_splitk_reduce(const GemmProblem &p, float *partial, int splits, hipStream_t s) {
+  KArgs g{};
+  g.M = p.M;
+  g.N = p.N;
+  g.K = p.K;
+  g.splits = splits;
+  g.epi = p.epi;
+  {
+    const Epilogue &e = p.epi;
+    const int mes = e.mask_dtype == IMBD_BF16 ? 2 : 4;
+    g.mask_vec = e.mask && ((uintptr_t)e.mask % (4 * mes) == 0) && (e.ldmask % 4 == 0);
+    g.bias_vec = e.bias && ((uintptr_t)e.bias % 16 == 0);
+  }
+  g.partial = partial;
+  g.ldp = partial_ld(p.M);
+  g.sstride = partial_split_stride(p.M, p.N);
+  return launch_reduce(p, g, s);
 }
 
 // ------------------------------------------------------------------ 3x3 conv tile

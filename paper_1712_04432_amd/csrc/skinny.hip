@@ -1,0 +1,333 @@
+// Forward and activation-gradient products of a fully connected layer for a batch of at
+// most 256 samples, bf16 operands (Sec. 1: Y = W X and Delta_X = W^T Delta_Y; App. A for
+// their block forms, which are the same products on a process's blocks).
+//
+// With B <= 256 these products stream the weight matrix once from HBM and do 2*B flops
+// per weight element. A workgroup owns a 64-row block of W against the whole batch
+// (up to 256 samples) over one K-range; K is split so that the grid fills the chip, and
+// the splits' fp32 partials are added in split order by the split-K reduce, which also
+// applies the bias/ReLU or mask epilogue. Both operands travel through LDS in 64-k slabs
+// written by buffer loads that go straight to LDS (no registers; out-of-range lanes
+// land as zeros), each load instruction covering whole 128-byte lines (8 rows x 128 B):
+// MFMA-layout loads into registers touch 16 half-lines per instruction and move less
+// than half as many bytes per clock from L2. Eight waves in three groups, each with its
+// own memory counter so that no group waits on another's loads:
+//  * waves 4-5 stream W through an eight-slot ring (up to six slabs in flight from HBM);
+//  * waves 6-7 stream the activation slab (L2 hits: the workgroups of one K-range run on
+//    one XCD) through a three-slot ring;
+//  * waves 0-3 read MFMA fragments from LDS: 16-byte reads, or for W used transposed
+//    (Delta_X) the gfx950 LDS transpose read, and accumulate the tile in registers.
+// Every group meets at one barrier per slab. Rows sit in LDS with their 16-byte chunks
+// XOR-swizzled so that each fragment read touches every bank once.
+
+#include <stdlib.h>
+
+#include "cdna4.h"
+
+namespace imbd {
+namespace {
+
+struct SkArgs {
+  const uint16_t *A;  // W: [M][lda] (k contiguous) or [K][lda] (m contiguous, A_TR)
+  const uint16_t *B;  // activations: [N][ldb], k contiguous
+  int64_t lda, ldb;
+  int M, N, K;
+  int k_split, splits, tiles_m;
+  float *partial;     // [split][N][ldp]
+  int64_t ldp, sstride;
+};
+
+constexpr int SK_BM = 64;                 // rows of the output (W) per workgroup
+constexpr int SK_KS = 64;                 // k per slab (128 bytes per row)
+constexpr int SK_NW = 8;                  // W ring slots
+constexpr int SK_NX = 3;                  // activation ring slots
+constexpr int SK_WSLOT = 64 * 128;        // 8 KB: 64 rows (KC) or 64 k-rows (TR) x 128 B
+
+// 16-byte chunk position of chunk c in row r of a slab read with 16-byte fragment reads:
+// the 16 rows of one read land on 16 distinct (row parity, chunk) bank groups.
+__device__ __forceinline__ int swz_kc(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// ... and of a W slab read with the transpose read (k-rows of 64 m-values).
+__device__ __forceinline__ int swz_tr(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
+
+// NB: the workgroup covers 64*NB samples; MMA wave w takes NB m-blocks and four
+// 16-sample blocks.
+template <bool A_TR, int NB>
+__global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int XROWS = 64 * NB;
+  constexpr int XSLOT = XROWS * 128;
+  constexpr int XRING = SK_NX * XSLOT;
+  __shared__ __attribute__((aligned(1024))) char smem[XRING + SK_NW * SK_WSLOT];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int G = gridDim.x;
+  int b = blockIdx.x;
+  // consecutive logical blocks (the tiles of one K-range) on one XCD
+  if ((G & 7) == 0) b = (b & 7) * (G >> 3) + (b >> 3);
+  const int split = b / a.tiles_m, m0 = (b - split * a.tiles_m) * SK_BM;
+  const int klo = split * a.k_split, krange = min(a.K, klo + a.k_split) - klo;
+  const int nsl = (krange + SK_KS - 1) / SK_KS;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
+  const uint32_t ldsx = lds0, ldsw = lds0 + XRING;
+
+  if (wave >= 6) {
+    // -------------------------------------------------- activation loaders (6, 7)
+    // Slab S: rows 0..XROWS-1 of the batch, k = klo + 64S ..; wave xw fills the 1 KB
+    // blocks 4NB*xw .. 4NB*xw + 4NB-1 of the slot (8 rows x 128 B each).
+    const int xw = wave - 6;
+    const i32x4 rb = buf_rsrc(a.B, (uint32_t)((int64_t)a.N * a.ldb * 2));
+    uint32_t base[4 * NB];
+    int kof[4 * NB];
+#pragma unroll
+    for (int q = 0; q < 4 * NB; ++q) {
+      const int r = 8 * (4 * NB * xw + q) + (lane >> 3);
+      const int c = (lane & 7) ^ swz_kc(r);
+      base[q] = (uint32_t)(((int64_t)r * a.ldb + klo + 8 * c) * 2);  // rows past N: out of range
+      kof[q] = 8 * c;
+    }
+    const uint32_t dst0 = ldsx + (uint32_t)(4 * NB * xw * 1024);
+    uint32_t slot = 0;  // ring slot of the next slab to issue
+    auto issue = [&](int S) {
+#pragma unroll
+      for (int q = 0; q < 4 * NB; ++q) {
+        const bool ok = S * SK_KS + kof[q] < krange;
+        dma16(rb, ok ? base[q] + (uint32_t)S * 128u : OOB, dst0 + slot + q * 1024);
+      }
+      slot = slot + XSLOT == XRING ? 0u : slot + XSLOT;
+    };
+#pragma unroll
+    for (int S = 0; S < SK_NX - 1; ++S) issue(S);
+    for (int S = 0; S < nsl; ++S) {
+      vm_barrier<4 * NB * (SK_NX - 2)>();  // slab S landed: B_S
+      issue(S + SK_NX - 1);                // into the slot of S-1
+    }
+    vm_barrier<0>();
+  } else if (wave >= 4) {
+    // ------------------------------------------------------------ W loaders (4, 5)
+    // KC slab: W rows m0..m0+63 x k = klo + 64S ..; TR slab: k-rows klo + 64S .. x
+    // m0..m0+63. Wave lw fills the 1 KB blocks 4lw..4lw+3 (8 rows x 128 B each).
+    const int lw = wave - 4;
+    const i32x4 ra = buf_rsrc(a.A, (uint32_t)((A_TR ? (int64_t)a.K : (int64_t)a.M) * a.lda * 2));
+    uint32_t base[4];
+    int kof[4];
+    bool okm[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = 8 * (4 * lw + q) + (lane >> 3);
+      if constexpr (!A_TR) {
+        const int c = (lane & 7) ^ swz_kc(r);
+        base[q] = (uint32_t)(((int64_t)(m0 + r) * a.lda + klo + 8 * c) * 2);  // rows past M: out of range
+        kof[q] = 8 * c;
+        okm[q] = true;
+      } else {
+        const int c = (lane & 7) ^ swz_tr(r);
+        base[q] = (uint32_t)(((int64_t)(klo + r) * a.lda + m0 + 8 * c) * 2);
+        kof[q] = r;
+        okm[q] = m0 + 8 * c < a.M;
+      }
+    }
+    const uint32_t sstep = A_TR ? (uint32_t)((int64_t)SK_KS * a.lda * 2) : (uint32_t)(SK_KS * 2);
+    const uint32_t dst0 = ldsw + (uint32_t)(4 * lw * 1024);
+    auto issue = [&](int S) {
+      const uint32_t dst = dst0 + (uint32_t)((S & (SK_NW - 1)) * SK_WSLOT);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bool ok = okm[q] && S * SK_KS + kof[q] < krange;
+        dma16(ra, ok ? base[q] + (uint32_t)S * sstep : OOB, dst + q * 1024);
+      }
+    };
+#pragma unroll
+    for (int S = 0; S < SK_NW - 1; ++S) issue(S);
+    for (int S = 0; S < nsl; ++S) {
+      vm_barrier<4 * (SK_NW - 2)>();  // slab S landed: B_S
+      issue(S + SK_NW - 1);           // into the slot of S-1
+    }
+    vm_barrier<0>();
+  } else {
+    // --------------------------------------------------------------- MMA group
+    constexpr int FM = NB;  // m-blocks per wave
+    const int fi = lane & 15, kg = lane >> 4;
+    const int nw = wave % NB, mw = wave / NB;
+    const int mb0 = FM * mw, nb0 = 4 * nw;  // first m-block and n-block of the wave
+    // fragment addresses within a slot for k-step 0 (k-step s reads KC chunk 4s + kg,
+    // TR k-rows 32s ..)
+    uint32_t fa[FM], fx[4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      if constexpr (!A_TR) {
+        fa[i] = (uint32_t)((16 * (mb0 + i) + fi) * 128);
+      } else {
+        // k-rows 8kg + fi/4 (+4) at columns 16i' + 4(fi%4) (i' = mb0 + i): the transpose
+        // read hands lane fi the four consecutive k of column 16i' + fi
+        const int r = 8 * kg + (fi >> 2);
+        const int c = (2 * (mb0 + i) + ((fi >> 1) & 1)) ^ swz_tr(r);
+        fa[i] = (uint32_t)(r * 128 + c * 16 + 8 * (fi & 1));
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fx[j] = (uint32_t)((16 * (nb0 + j) + fi) * 128);
+    const int sw = swz_kc(fi);  // rows 16i + fi all have this swizzle
+
+    f32x4 acc[FM][4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    bf16x8 wa[2][FM], xb[2][4];
+    auto read = [&](uint32_t ws, uint32_t xs, int s, bf16x8 (&wd)[FM], bf16x8 (&xd)[4]) {
+      const uint32_t co = (uint32_t)(((4 * s + kg) ^ sw) * 16);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        if constexpr (!A_TR) {
+          wd[i] = __builtin_bit_cast(bf16x8, *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(ws + fa[i] + co));
+        } else {
+          lds_i16x4 *p = (lds_i16x4 *)(uintptr_t)(ws + fa[i] + (uint32_t)(s * 4096));
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p);
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p + 4 * 128 / 8);
+          wd[i] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        xd[j] = __builtin_bit_cast(bf16x8, *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(xs + fx[j] + co));
+    };
+    auto mma = [&](const bf16x8 (&wf)[FM], const bf16x8 (&xf)[4]) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], xf[j], acc[i][j], 0, 0, 0);
+    };
+
+    uint32_t ws = ldsw, xs = ldsx;  // slots of the slab being read
+    lds_barrier();                  // B_0: slab 0 landed
+    read(ws, xs, 0, wa[0], xb[0]);
+    // Each k-step issues the fragment reads of the next one before its own MFMAs, so
+    // that the reads land behind 16 MFMAs; the scheduling barriers keep that order.
+    for (int S = 0; S < nsl; ++S) {
+      read(ws, xs, 1, wa[1], xb[1]);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(wa[0], xb[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      // every read of slab S has landed: publish S+1, free S
+      lds_barrier();  // B_{S+1}
+      ws = ldsw + (uint32_t)(((S + 1) & (SK_NW - 1)) * SK_WSLOT);
+      xs = xs + XSLOT == ldsx + XRING ? ldsx : xs + XSLOT;
+      read(ws, xs, 0, wa[0], xb[0]);  // past the last slab this reads a spent slot, unused
+      __builtin_amdgcn_sched_barrier(0);
+      mma(wa[1], xb[1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+
+    // ---- stage the tile: element (n, m) at float n*64 + 4*((m/4) ^ (n%16)) + m%4.
+    // The activation ring is free: every wave has passed B_nsl.
+    float *stg = reinterpret_cast<float *>(smem);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int n = 16 * (nb0 + j) + fi, u = 4 * (mb0 + i) + kg;
+        *reinterpret_cast<f32x4 *>(stg + n * 64 + 4 * (u ^ (n & 15))) = acc[i][j];
+      }
+  }
+  lds_barrier();
+  // ---- partial tile out: 16 threads per 256-byte row
+  const float *stg = reinterpret_cast<const float *>(smem);
+  float *dst = a.partial + (int64_t)split * a.sstride + m0;
+  const int u = tid & 15;
+#pragma unroll
+  for (int p = 0; p < 2 * NB; ++p) {
+    const int n = 32 * p + (tid >> 4);
+    if (n < a.N) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + n * 64 + 4 * (u ^ (n & 15)));
+      *reinterpret_cast<f32x4 *>(dst + (int64_t)n * a.ldp + 4 * u) = v;
+    }
+  }
+}
+
+int nb_for(int N) { return N <= 64 ? 1 : N <= 128 ? 2 : 4; }
+
+int env_splits() {
+  const char *s = getenv("IMBD_SKINNY_SPLITS");
+  return s ? atoi(s) : 0;
+}
+
+}  // namespace
+
+bool skinny_fits(const GemmProblem &p) {
+  auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
+  const int64_t arows = p.a_kc ? p.M : p.K;
+  return p.dtype == IMBD_BF16 && p.b_kc && p.epi.mode == EPI_STORE && p.db_mode == 0 && p.N >= 1 &&
+         p.N <= 256 && p.M >= 1 && p.K >= 8 && p.K % 8 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+         al(p.A, 16) && al(p.B, 16) && (arows + SK_KS + SK_BM) * p.lda * 2 < ((int64_t)1 << 31) &&
+         ((int64_t)256 * p.ldb + p.K + SK_KS) * 2 < ((int64_t)1 << 31) && (p.a_kc || p.M % 8 == 0);
+}
+
+// Splits: fill the chip, traded against the partials' traffic (each split writes an
+// fp32 M x N partial, which the reduce reads back). Modelled time of a split count: the
+// larger of the HBM time (W, the activations once, the partials written and read) and
+// the time of one workgroup (slabs at ~900 cycles each plus ~12k cycles of fill and
+// partial write-out), times the rounds of workgroups over 256 CUs.
+void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
+  const int tiles = (p.M + SK_BM - 1) / SK_BM;
+  const double hbm = 5.0e12, clk = 2.1e9, slab_clk = 900.0, fill_clk = 12000.0;
+  int best_s = 1;
+  double best_t = 1e30;
+  const int forced = env_splits();
+  for (int s = 1; s <= 64; ++s) {
+    const int ks = ((p.K + s - 1) / s + SK_KS - 1) / SK_KS * SK_KS;
+    if ((p.K + ks - 1) / ks != s) continue;
+    const int blocks = tiles * s;
+    if (blocks > 65535) break;
+    const double bytes = 2.0 * p.M * p.K + 2.0 * p.N * p.K + 8.0 * s * (double)p.M * p.N;
+    const int rounds = (blocks + 255) / 256;
+    const double t_cu = rounds * ((ks / SK_KS) * slab_clk + fill_clk) / clk;
+    const double t = bytes / hbm > t_cu ? bytes / hbm : t_cu;
+    if (forced > 0 ? s == forced : t < best_t * 0.98) {
+      best_t = t;
+      best_s = s;
+    }
+  }
+  const int ks = ((p.K + best_s - 1) / best_s + SK_KS - 1) / SK_KS * SK_KS;
+  *k_split_out = ks;
+  *splits_out = (p.K + ks - 1) / ks;
+}
+
+int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
+  int splits, k_split;
+  skinny_plan(p, &splits, &k_split);
+  SkArgs g;
+  g.A = reinterpret_cast<const uint16_t *>(p.A);
+  g.B = reinterpret_cast<const uint16_t *>(p.B);
+  g.lda = p.lda;
+  g.ldb = p.ldb;
+  g.M = p.M;
+  g.N = p.N;
+  g.K = p.K;
+  g.k_split = k_split;
+  g.splits = splits;
+  g.tiles_m = (p.M + SK_BM - 1) / SK_BM;
+  g.partial = reinterpret_cast<float *>(ws);
+  g.ldp = partial_ld(p.M);
+  g.sstride = partial_split_stride(p.M, p.N);
+  const int grid = g.tiles_m * splits;
+  const int nb = nb_for(p.N);
+  {
+    LaunchTimer t(p.kclass, p.layer, s);
+    if (p.a_kc) {
+      if (nb == 1) hipLaunchKernelGGL((skinny_kernel<false, 1>), dim3(grid), dim3(512), 0, s, g);
+      else if (nb == 2) hipLaunchKernelGGL((skinny_kernel<false, 2>), dim3(grid), dim3(512), 0, s, g);
+      else hipLaunchKernelGGL((skinny_kernel<false, 4>), dim3(grid), dim3(512), 0, s, g);
+    } else {
+      if (nb == 1) hipLaunchKernelGGL((skinny_kernel<true, 1>), dim3(grid), dim3(512), 0, s, g);
+      else if (nb == 2) hipLaunchKernelGGL((skinny_kernel<true, 2>), dim3(grid), dim3(512), 0, s, g);
+      else hipLaunchKernelGGL((skinny_kernel<true, 4>), dim3(grid), dim3(512), 0, s, g);
+    }
+  }
+  const int rc = check_launch("skinny");
+  if (rc != IMBD_OK) return rc;
+  return run_splitk_reduce(p, g.partial, splits, s);
+}
+
+}  // namespace imbd
