@@ -93,14 +93,13 @@ GemmPlan gemm_plan(const GemmProblem &p);
 // powers of two.
 inline int64_t partial_ld(int M) { return ((int64_t)M + 7) / 8 * 8 + 64; }
 inline int64_t partial_split_stride(int M, int N) { return (int64_t)N * partial_ld(M) + 1088; }
-// Adds `splits` partial sums in split order and applies p's (store) epilogue.
-int run_splitk_reduce(const GemmProblem &p, float *partial, int splits, hipStream_t s);
 // Forward / Delta_X products for batches up to 256 (bf16): whether the skinny kernel
-// takes the problem, its K split, and the launch (kernel + reduce; ws holds the plan's
-// partials).
+// takes the problem, its K split, the launch (kernel + its reduce) and the bytes of
+// partial sums it needs in ws.
 bool skinny_fits(const GemmProblem &p);
 void skinny_plan(const GemmProblem &p, int *splits, int *k_split);
 int run_skinny(const GemmProblem &p, void *ws, hipStream_t s);
+size_t skinny_ws_bytes(const GemmProblem &p);
 // The persistent fused weight-gradient + update kernel (bf16, K <= 256): whether it
 // takes the problem, and the launch.
 bool dw_sgd_fits(const GemmProblem &p);

@@ -848,7 +848,7 @@ GemmPlan gemm_plan(const GemmProblem &p) {
     pl.cfg = -1;
     pl.bm = 64;
     pl.bn = 256;
-    pl.ws_bytes = (size_t)pl.splits * (size_t)partial_split_stride(p.M, p.N) * sizeof(float);
+    pl.ws_bytes = skinny_ws_bytes(p);
     return pl;
   }
   const int esz = p.dtype == IMBD_BF16 ? 2 : 4;
@@ -989,25 +989,6 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   }
   if (pl.splits > 1) rc = launch_reduce(p, g, s);
   return rc;
-}
-
-int run_splitk_reduce(const GemmProblem &p, float *partial, int splits, hipStream_t s) {
-  KArgs g{};
-  g.M = p.M;
-  g.N = p.N;
-  g.K = p.K;
-  g.splits = splits;
-  g.epi = p.epi;
-  {
-    const Epilogue &e = p.epi;
-    const int mes = e.mask_dtype == IMBD_BF16 ? 2 : 4;
-    g.mask_vec = e.mask && ((uintptr_t)e.mask % (4 * mes) == 0) && (e.ldmask % 4 == 0);
-    g.bias_vec = e.bias && ((uintptr_t)e.bias % 16 == 0);
-  }
-  g.partial = partial;
-  g.ldp = partial_ld(p.M);
-  g.sstride = partial_split_stride(p.M, p.N);
-  return launch_reduce(p, g, s);
 }
 
 // ------------------------------------------------------------------ 3x3 conv tile

@@ -33,9 +33,15 @@ struct SkArgs {
   int64_t lda, ldb;
   int M, N, K;
   int k_split, splits, tiles_m;
-  float *partial;     // [split][N][ldp]
-  int64_t ldp, sstride;
+  float *partial;     // [split][tile][N][64]: one contiguous block per workgroup
+  int64_t tpitch, sstride;
 };
+
+// Partial-sum layout: each workgroup's 64 x N tile is one contiguous block (a tile pitch
+// of N*64 floats plus 64, a split pitch off powers of two), so the write-out and the
+// reduce stream whole blocks.
+inline int64_t sk_tile_pitch(int N) { return (int64_t)N * 64 + 64; }
+inline int64_t sk_split_pitch(int M, int N) { return (int64_t)((M + 63) / 64) * sk_tile_pitch(N) + 1088; }
 
 constexpr int SK_BM = 64;                 // rows of the output (W) per workgroup
 constexpr int SK_KS = 64;                 // k per slab (128 bytes per row)
@@ -130,7 +136,7 @@ __global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
     const uint32_t sstep = A_TR ? (uint32_t)((int64_t)SK_KS * a.lda * 2) : (uint32_t)(SK_KS * 2);
     const uint32_t dst0 = ldsw + (uint32_t)(4 * lw * 1024);
     auto issue = [&](int S) {
-      const uint32_t dst = dst0 + (uint32_t)((S & (SK_NW - 1)) * SK_WSLOT);
+      const uint32_t dst = dst0 + (uint32_t)((S % SK_NW) * SK_WSLOT);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const bool ok = okm[q] && S * SK_KS + kof[q] < krange;
@@ -212,7 +218,7 @@ __global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
       __builtin_amdgcn_sched_barrier(0);
       // every read of slab S has landed: publish S+1, free S
       lds_barrier();  // B_{S+1}
-      ws = ldsw + (uint32_t)(((S + 1) & (SK_NW - 1)) * SK_WSLOT);
+      ws = ldsw + (uint32_t)(((S + 1) % SK_NW) * SK_WSLOT);
       xs = xs + XSLOT == ldsx + XRING ? ldsx : xs + XSLOT;
       read(ws, xs, 0, wa[0], xb[0]);  // past the last slab this reads a spent slot, unused
       __builtin_amdgcn_sched_barrier(0);
@@ -232,16 +238,96 @@ __global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
       }
   }
   lds_barrier();
-  // ---- partial tile out: 16 threads per 256-byte row
+  // ---- partial tile out: one contiguous block, 16 threads per 256-byte row
   const float *stg = reinterpret_cast<const float *>(smem);
-  float *dst = a.partial + (int64_t)split * a.sstride + m0;
+  float *dst = a.partial + (int64_t)split * a.sstride + (int64_t)(m0 / SK_BM) * a.tpitch;
   const int u = tid & 15;
 #pragma unroll
   for (int p = 0; p < 2 * NB; ++p) {
     const int n = 32 * p + (tid >> 4);
     if (n < a.N) {
       const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + n * 64 + 4 * (u ^ (n & 15)));
-      *reinterpret_cast<f32x4 *>(dst + (int64_t)n * a.ldp + 4 * u) = v;
+      *reinterpret_cast<f32x4 *>(dst + n * 64 + 4 * u) = v;
+    }
+  }
+}
+
+struct SkReduceArgs {
+  const float *partial;
+  int64_t tpitch, sstride;
+  int M, N, splits;
+  Epilogue epi;
+};
+
+// Adds the splits' partials in split order (the same order and arithmetic as the
+// split-K reduce of the tiled products) and applies the store epilogue:
+// out(m, n) = [mask(m, n) > 0] * relu?(alpha * sum + bias[m]). Eight consecutive m of one
+// sample per thread; VEC: every access is whole and aligned (checked on the host).
+template <bool VEC>
+__global__ void __launch_bounds__(256) skinny_reduce(SkReduceArgs g) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int tile = (int)(t / ((int64_t)g.N * 8));
+  const int r = (int)(t - (int64_t)tile * g.N * 8);
+  const int n = r >> 3, m = tile * 64 + 8 * (r & 7);
+  if (n >= g.N || m >= g.M) return;
+  const Epilogue &e = g.epi;
+  const float *p = g.partial + (int64_t)tile * g.tpitch + n * 64 + (m & 63);
+  f32x4 a0 = *reinterpret_cast<const f32x4 *>(p);
+  f32x4 a1 = *reinterpret_cast<const f32x4 *>(p + 4);
+  for (int s0 = 1; s0 < g.splits; s0 += 4) {
+    f32x4 q0[4], q1[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (s0 + u < g.splits) {
+        const float *q = p + (int64_t)(s0 + u) * g.sstride;
+        q0[u] = *reinterpret_cast<const f32x4 *>(q);
+        q1[u] = *reinterpret_cast<const f32x4 *>(q + 4);
+      }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (s0 + u < g.splits) {
+        a0 += q0[u];
+        a1 += q1[u];
+      }
+  }
+  const float v[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+  const int cnt = VEC ? 8 : min(8, g.M - m);
+  float x[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if (i < cnt) {
+      float y = e.alpha * v[i] + (e.bias ? e.bias[m + i] : 0.0f);
+      if (e.relu) y = y > 0.0f ? y : 0.0f;
+      if (e.mask) {
+        const int64_t off = (int64_t)n * e.ldmask + m + i;
+        const float mk = e.mask_dtype == IMBD_BF16 ? bf16_to_f32(reinterpret_cast<const uint16_t *>(e.mask)[off])
+                                                   : reinterpret_cast<const float *>(e.mask)[off];
+        if (!(mk > 0.0f)) y = 0.0f;
+      }
+      x[i] = y;
+    }
+  }
+  if (e.out_dtype == IMBD_BF16) {
+    uint16_t *o = reinterpret_cast<uint16_t *>(e.out) + (int64_t)n * e.ldo + m;
+    if constexpr (VEC) {
+      u32x4 pk;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pk[i] = (uint32_t)f32_to_bf16(x[2 * i]) | ((uint32_t)f32_to_bf16(x[2 * i + 1]) << 16);
+      *reinterpret_cast<u32x4 *>(o) = pk;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (i < cnt) o[i] = f32_to_bf16(x[i]);
+    }
+  } else {
+    float *o = reinterpret_cast<float *>(e.out) + (int64_t)n * e.ldo + m;
+    if constexpr (VEC) {
+      *reinterpret_cast<f32x4 *>(o) = f32x4{x[0], x[1], x[2], x[3]};
+      *reinterpret_cast<f32x4 *>(o + 4) = f32x4{x[4], x[5], x[6], x[7]};
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (i < cnt) o[i] = x[i];
     }
   }
 }
@@ -309,8 +395,8 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
   g.splits = splits;
   g.tiles_m = (p.M + SK_BM - 1) / SK_BM;
   g.partial = reinterpret_cast<float *>(ws);
-  g.ldp = partial_ld(p.M);
-  g.sstride = partial_split_stride(p.M, p.N);
+  g.tpitch = sk_tile_pitch(p.N);
+  g.sstride = sk_split_pitch(p.M, p.N);
   const int grid = g.tiles_m * splits;
   const int nb = nb_for(p.N);
   {
@@ -325,9 +411,34 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
       else hipLaunchKernelGGL((skinny_kernel<true, 4>), dim3(grid), dim3(512), 0, s, g);
     }
   }
-  const int rc = check_launch("skinny");
+  int rc = check_launch("skinny");
   if (rc != IMBD_OK) return rc;
-  return run_splitk_reduce(p, g.partial, splits, s);
+  SkReduceArgs r;
+  r.partial = g.partial;
+  r.tpitch = g.tpitch;
+  r.sstride = g.sstride;
+  r.M = p.M;
+  r.N = p.N;
+  r.splits = splits;
+  r.epi = p.epi;
+  const Epilogue &e = p.epi;
+  auto al = [](const void *q, int a) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % a) == 0; };
+  const bool vec = p.M % 8 == 0 && al(e.out, 16) && e.ldo % 8 == 0 &&
+                   (e.mask == nullptr || (al(e.mask, 16) && e.ldmask % 8 == 0));
+  const int64_t threads = (int64_t)g.tiles_m * p.N * 8;
+  const unsigned blocks = (unsigned)((threads + 255) / 256);
+  {
+    LaunchTimer t(IMBD_K_SPLITK, p.layer, s);
+    if (vec) hipLaunchKernelGGL(skinny_reduce<true>, dim3(blocks), dim3(256), 0, s, r);
+    else hipLaunchKernelGGL(skinny_reduce<false>, dim3(blocks), dim3(256), 0, s, r);
+  }
+  return check_launch("skinny_reduce");
+}
+
+size_t skinny_ws_bytes(const GemmProblem &p) {
+  int splits, k_split;
+  skinny_plan(p, &splits, &k_split);
+  return (size_t)splits * (size_t)sk_split_pitch(p.M, p.N) * sizeof(float);
 }
 
 }  // namespace imbd
