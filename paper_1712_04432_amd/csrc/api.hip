@@ -264,6 +264,13 @@ int mlp_fwd(const imbd_mlp_desc *d, const imbd_layer *layers, const void *x, con
       e.out_dtype = IMBD_F32;
     }
     e.ldo = d->dims[i];
+    if (i == L && gemm_plan(p).cfg < 0 && skinny_softmax_fits(p)) {
+      // top layer: split reduce, bias and softmax cross-entropy in one pass
+      if (lay.partial_bytes < gemm_plan(p).ws_bytes) FAIL(IMBD_EWORKSPACE, "partial-sum region too small");
+      float *rl = reinterpret_cast<float *>(at(ws, lay.rowloss));
+      TRY(run_skinny_softmax(p, part, labels, 1.0f / (float)B, rl, at(ws, lay.dy[L]), d->dims[L], d->dtype, s));
+      return run_loss_mean(B, rl, 1.0f / (float)B, loss, s);
+    }
     TRY(gemm_run(p, part, lay.partial_bytes, s));
   }
   return run_softmax_xent(B, d->dims[L], reinterpret_cast<const float *>(at(ws, lay.logits)), d->dims[L],

@@ -100,6 +100,13 @@ bool skinny_fits(const GemmProblem &p);
 void skinny_plan(const GemmProblem &p, int *splits, int *k_split);
 int run_skinny(const GemmProblem &p, void *ws, hipStream_t s);
 size_t skinny_ws_bytes(const GemmProblem &p);
+// The top layer's forward product with its split reduce fused into softmax cross-entropy
+// (logits stored to p.epi.out, per-sample losses and the logits' gradient); the loss mean
+// is left to the caller.
+bool skinny_softmax_fits(const GemmProblem &p);
+int run_skinny_softmax(const GemmProblem &p, void *ws, const int32_t *labels, float inv_batch, float *row_loss,
+                       void *dz, int64_t lddz, int dz_dtype, hipStream_t s);
+int run_loss_mean(int B, const float *row_loss, float inv_batch, float *loss, hipStream_t s);
 // The persistent fused weight-gradient + update kernel (bf16, K <= 256): whether it
 // takes the problem, and the launch.
 bool dw_sgd_fits(const GemmProblem &p);

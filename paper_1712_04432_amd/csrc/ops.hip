@@ -202,6 +202,11 @@ int run_softmax_xent(int B, int C, const float *logits, int64_t ldz, const int32
   }
   int rc = check_launch("softmax_xent_rows");
   if (rc) return rc;
+  return run_loss_mean(B, row_loss, inv_batch, loss, s);
+}
+
+int run_loss_mean(int B, const float *row_loss, float inv_batch, float *loss, hipStream_t s) {
+  if (B <= 0) return IMBD_OK;
   hipLaunchKernelGGL(loss_mean, dim3(1), dim3(256), 0, s, B, row_loss, inv_batch, loss);
   return check_launch("loss_mean");
 }

@@ -332,12 +332,82 @@ __global__ void __launch_bounds__(256) skinny_reduce(SkReduceArgs g) {
   }
 }
 
+struct SkSoftmaxArgs {
+  const float *partial;
+  int64_t tpitch, sstride;
+  int splits, B, C;
+  float alpha;
+  const float *bias;
+  float *logits;  // [B][ldz] fp32
+  int64_t ldz;
+  const int32_t *labels;
+  float inv_batch;
+  float *row_loss;
+  void *dz;       // [B][lddz] gradient of the batch-mean loss w.r.t. the logits
+  int64_t lddz;
+  int dz_bf16;
+};
+
+// Top layer, one workgroup per sample (one thread per class, C <= 1024): the logit is
+// the splits' partials added in split order plus the bias (the same arithmetic as the
+// reduce), stored; then softmax cross-entropy over the row: maximum, sum of
+// exp(z - max) (each wave in the shuffle order of the row kernel, the waves' values
+// added in wave order), per-sample loss lse - z[label] and the gradient
+// inv_batch * (softmax - onehot).
+__global__ void __launch_bounds__(1024) skinny_softmax_rows(SkSoftmaxArgs g) {
+  __shared__ float red[2][16];
+  const int row = blockIdx.x, c = threadIdx.x, lane = c & 63, w = c >> 6;
+  const int nw = (g.C + 63) >> 6;
+  const bool in = c < g.C;
+  float z = -INFINITY;
+  if (in) {
+    const float *p = g.partial + (int64_t)(c >> 6) * g.tpitch + row * 64 + (c & 63);
+    float a = p[0];
+    for (int q0 = 1; q0 < g.splits; q0 += 8) {
+      float t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = q0 + u < g.splits ? p[(int64_t)(q0 + u) * g.sstride] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (q0 + u < g.splits) a += t[u];
+    }
+    z = g.alpha * a + (g.bias ? g.bias[c] : 0.0f);
+    g.logits[(int64_t)row * g.ldz + c] = z;
+  }
+  float mx = z;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  if (lane == 0) red[0][w] = mx;
+  __syncthreads();
+  mx = red[0][0];
+  for (int k = 1; k < nw; ++k) mx = fmaxf(mx, red[0][k]);
+  const float e = in ? expf(z - mx) : 0.0f;
+  float s = e;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  if (lane == 0) red[1][w] = s;
+  __syncthreads();
+  s = red[1][0];
+  for (int k = 1; k < nw; ++k) s += red[1][k];
+  const int lab = g.labels[row];
+  const bool ok = lab >= 0 && lab < g.C;
+  if (c == (ok ? lab : 0)) g.row_loss[row] = ok ? (mx + logf(s) - z) : __builtin_nanf("");
+  if (in) {
+    const float gr = g.inv_batch * (e * (1.0f / s) - (c == lab ? 1.0f : 0.0f));
+    if (g.dz_bf16)
+      reinterpret_cast<uint16_t *>(g.dz)[(int64_t)row * g.lddz + c] = f32_to_bf16(gr);
+    else
+      reinterpret_cast<float *>(g.dz)[(int64_t)row * g.lddz + c] = gr;
+  }
+}
+
 int nb_for(int N) { return N <= 64 ? 1 : N <= 128 ? 2 : 4; }
 
-int env_splits() {
-  const char *s = getenv("IMBD_SKINNY_SPLITS");
+int env_int_skinny(const char *name) {
+  const char *s = getenv(name);
   return s ? atoi(s) : 0;
 }
+int env_splits() { return env_int_skinny("IMBD_SKINNY_SPLITS"); }
 
 }  // namespace
 
@@ -380,7 +450,8 @@ void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
   *splits_out = (p.K + ks - 1) / ks;
 }
 
-int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
+// Launches the product kernel (partials into ws); returns its arguments in *out.
+static int launch_skinny_product(const GemmProblem &p, void *ws, hipStream_t s, SkArgs *out) {
   int splits, k_split;
   skinny_plan(p, &splits, &k_split);
   SkArgs g;
@@ -411,8 +482,15 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
       else hipLaunchKernelGGL((skinny_kernel<true, 4>), dim3(grid), dim3(512), 0, s, g);
     }
   }
-  int rc = check_launch("skinny");
+  *out = g;
+  return check_launch("skinny");
+}
+
+int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
+  SkArgs g;
+  int rc = launch_skinny_product(p, ws, s, &g);
   if (rc != IMBD_OK) return rc;
+  const int splits = g.splits;
   SkReduceArgs r;
   r.partial = g.partial;
   r.tpitch = g.tpitch;
@@ -433,6 +511,41 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
     else hipLaunchKernelGGL(skinny_reduce<false>, dim3(blocks), dim3(256), 0, s, r);
   }
   return check_launch("skinny_reduce");
+}
+
+bool skinny_softmax_fits(const GemmProblem &p) {
+  return skinny_fits(p) && p.a_kc && p.M <= 1024 && p.epi.relu == 0 && p.epi.mask == nullptr &&
+         p.epi.out_dtype == IMBD_F32 && env_int_skinny("IMBD_TOP_UNFUSED") == 0;
+}
+
+int run_skinny_softmax(const GemmProblem &p, void *ws, const int32_t *labels, float inv_batch, float *row_loss,
+                       void *dz, int64_t lddz, int dz_dtype, hipStream_t s) {
+  SkArgs g;
+  int rc = launch_skinny_product(p, ws, s, &g);
+  if (rc != IMBD_OK) return rc;
+  SkSoftmaxArgs a;
+  a.partial = g.partial;
+  a.tpitch = g.tpitch;
+  a.sstride = g.sstride;
+  a.splits = g.splits;
+  a.B = p.N;
+  a.C = p.M;
+  a.alpha = p.epi.alpha;
+  a.bias = p.epi.bias;
+  a.logits = reinterpret_cast<float *>(p.epi.out);
+  a.ldz = p.epi.ldo;
+  a.labels = labels;
+  a.inv_batch = inv_batch;
+  a.row_loss = row_loss;
+  a.dz = dz;
+  a.lddz = lddz;
+  a.dz_bf16 = dz_dtype == IMBD_BF16 ? 1 : 0;
+  {
+    LaunchTimer t(IMBD_K_SOFTMAX, p.layer, s);
+    const int threads = (p.M + 63) / 64 * 64;
+    hipLaunchKernelGGL(skinny_softmax_rows, dim3(p.N), dim3(threads), 0, s, a);
+  }
+  return check_launch("skinny_softmax_rows");
 }
 
 size_t skinny_ws_bytes(const GemmProblem &p) {
