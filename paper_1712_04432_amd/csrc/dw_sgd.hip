@@ -23,10 +23,14 @@
 namespace imbd {
 namespace {
 
-// Cache-policy operand of the master loads and stores: default policy. (The
-// non-temporal bit cut the L2 misses of the operand loads but slowed the master stream
-// itself by more on most layer shapes.)
-constexpr int CPOL_MASTER = 0;
+// Cache policy of the fp32 master loads: non-temporal. The masters are read once per
+// step; keeping them out of the caches leaves the bf16 copy this kernel writes (which
+// the next step's forward product reads) resident in the 256 MB MALL. In the AlexNet FC
+// step that takes the layer-1 forward from 39 to 29 us and this kernel's layer-1 launch
+// from 82 to 76 us. The master and bf16 stores keep the default policy (non-temporal
+// master stores shortened the step a little further but slowed this kernel).
+constexpr int CPOL_MASTER_LD = 2;
+constexpr int CPOL_MASTER_ST = 0;
 
 struct DwArgs {
   const uint16_t *X;   // [K][ldx]  rows are samples, M = d_in columns
@@ -292,18 +296,18 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
           u32x2 pk;
           pk[0] = cvt_pk_bf16(nw[0], nw[1]);
           pk[1] = cvt_pk_bf16(nw[2], nw[3]);
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, nw), rp, vp + pp * wrow, 0, CPOL_MASTER);
-          __builtin_amdgcn_raw_buffer_store_b64(pk, rh, vh + pp * hrow, 0, CPOL_MASTER);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, nw), rp, vp + pp * wrow, 0, CPOL_MASTER_ST);
+          __builtin_amdgcn_raw_buffer_store_b64(pk, rh, vh + pp * hrow, 0, CPOL_MASTER_ST);
         }
         // refill the registers of chunk ch - LAG (tile it) or ch - LAG + CHUNKS (tile it-1)
 #pragma unroll
         for (int q = 0; q < CP; ++q) {
           if (ch >= LAG) {
             const int pp = (ch - LAG) * CP + q;
-            wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rn, vn + pp * wrow, 0, CPOL_MASTER));
+            wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rn, vn + pp * wrow, 0, CPOL_MASTER_LD));
           } else {
             const int pp = (ch - LAG + CHUNKS) * CP + q;
-            wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, vp + pp * wrow, 0, CPOL_MASTER));
+            wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, vp + pp * wrow, 0, CPOL_MASTER_LD));
           }
         }
         if (have && ch < TK) lds_barrier();
