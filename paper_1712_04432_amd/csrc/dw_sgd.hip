@@ -68,10 +68,16 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
   const int G = gridDim.x;  // a multiple of tiles_n: every tile of a workgroup has the same column block
   int b = blockIdx.x;
   if ((G & 7) == 0) b = (b & 7) * (G >> 3) + (b >> 3);
-  const int nmy = b < tiles ? (tiles - 1 - b) / G + 1 : 0;
+  // The gpb workgroups of a column block share its row blocks; the k-th row block of the
+  // one with index grp is gpb*k + (grp + k) % gpb, so that every workgroup visits every
+  // column offset modulo gpb row blocks. (A fixed offset per workgroup left some of them
+  // on slow address classes: layer-1 finish times spread 53-73 us, now 62-70 us.)
+  const int gpb = G / a.tiles_n, grp = b / a.tiles_n;
+  const int full = a.tiles_m / gpb, rem = a.tiles_m % gpb;
+  const int nmy = b < tiles ? full + ((grp + full) % gpb < rem ? 1 : 0) : 0;
   const int TK = (a.K + BK - 1) / BK;
   const int n0 = (b % a.tiles_n) * BN;
-  auto tile_m0 = [&](int it) { return ((b + it * G) / a.tiles_n) * BM; };
+  auto tile_m0 = [&](int it) { return (gpb * it + (grp + it) % gpb) * BM; };
 
   if (tid < NTM) {
     // ------------------------------------------------------------------ MMA group
@@ -190,7 +196,7 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
 
     // Bias gradient: the column sums of Delta_Y, once, by the workgroups whose first tile
     // is in the first row block. Lanes l and l+32 of a wave split the batch of one column.
-    if (a.db_mode != 0 && b < a.tiles_n && nmy > 0) {
+    if (a.db_mode != 0 && b < tiles && grp == 0) {
       const int c = wave * 32 + (lane & 31), half = lane >> 5;
       const int kh = (KMAX / 2);
       float sum = 0.f;
