@@ -43,6 +43,7 @@ struct SkArgs {
 inline int64_t sk_tile_pitch(int N) { return (int64_t)N * 64 + 64; }
 inline int64_t sk_split_pitch(int M, int N) { return (int64_t)((M + 63) / 64) * sk_tile_pitch(N) + 1088; }
 
+constexpr int CPOL_SC1 = 16;              // cache-policy operand of the raw buffer builtins: sc1
 constexpr int SK_BM = 64;                 // rows of the output (W) per workgroup
 constexpr int SK_KS = 64;                 // k per slab (128 bytes per row)
 constexpr int SK_NW = 8;                  // W ring slots
@@ -240,16 +241,19 @@ __global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
       }
   }
   lds_barrier();
-  // ---- partial tile out: one contiguous block, 16 threads per 256-byte row
+  // ---- partial tile out: one contiguous block, 16 threads per 256-byte row. Device-scope
+  // stores (sc1) write through the XCD's L2, so the partials do not sit there dirty until
+  // the end-of-kernel writeback (measured 1-2 us faster per product than default stores).
   const float *stg = reinterpret_cast<const float *>(smem);
   float *dst = a.partial + (int64_t)split * a.sstride + (int64_t)(m0 / SK_BM) * a.tpitch;
+  const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(dst, 0, (int)(a.tpitch * 4), BUF_DW3);
   const int u = tid & 15;
 #pragma unroll
   for (int p = 0; p < 2 * NB; ++p) {
     const int n = 32 * p + (tid >> 4);
     if (n < a.N) {
       const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + n * 64 + 4 * (u ^ (n & 15)));
-      *reinterpret_cast<f32x4 *>(dst + n * 64 + 4 * u) = v;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), prs, (uint32_t)((n * 64 + 4 * u) * 4), 0, CPOL_SC1);
     }
   }
 }
@@ -422,14 +426,16 @@ bool skinny_fits(const GemmProblem &p) {
          ((int64_t)256 * p.ldb + p.K + SK_KS) * 2 < ((int64_t)1 << 31) && (p.a_kc || p.M % 8 == 0);
 }
 
-// Splits: fill the chip, traded against the partials' traffic (each split writes an
-// fp32 M x N partial, which the reduce reads back). Modelled time of a split count: the
-// larger of the HBM time (W, the activations once, the partials written and read) and
-// the time of one workgroup (slabs at ~900 cycles each plus ~12k cycles of fill and
-// partial write-out), times the rounds of workgroups over 256 CUs.
+// Splits: fill the chip, traded against the partials (each split writes an fp32 M x N
+// partial, which the reduce reads back). Modelled time of a split count: the larger of
+// the HBM time of the operands and the time of one workgroup (~0.5 us per slab plus ~3 us
+// of fill and write-out) times the rounds of workgroups over 256 CUs, plus ~1 us per MB
+// of partials for writing them out and reading them back (fitted to timings of the
+// AlexNet FC products at B = 256: more, shorter workgroups lose once the partials grow,
+// e.g. the 1000 x 4096 forward is fastest at 6 splits on 96 workgroups).
 void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
   const int tiles = (p.M + SK_BM - 1) / SK_BM;
-  const double hbm = 5.0e12, clk = 2.1e9, slab_clk = 900.0, fill_clk = 12000.0;
+  const double hbm = 5.0e12, clk = 2.1e9, slab_clk = 1050.0, fill_clk = 6300.0, part_bw = 1.0e12;
   int best_s = 1;
   double best_t = 1e30;
   const int forced = env_splits();
@@ -438,10 +444,11 @@ void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
     if ((p.K + ks - 1) / ks != s) continue;
     const int blocks = tiles * s;
     if (blocks > 65535) break;
-    const double bytes = 2.0 * p.M * p.K + 2.0 * p.N * p.K + 8.0 * s * (double)p.M * p.N;
+    const double bytes = 2.0 * p.M * p.K + 2.0 * p.N * p.K;
+    const double part = 4.0 * s * (double)tiles * SK_BM * p.N;
     const int rounds = (blocks + 255) / 256;
     const double t_cu = rounds * ((ks / SK_KS) * slab_clk + fill_clk) / clk;
-    const double t = bytes / hbm > t_cu ? bytes / hbm : t_cu;
+    const double t = (bytes / hbm > t_cu ? bytes / hbm : t_cu) + part / part_bw;
     if (forced > 0 ? s == forced : t < best_t * 0.98) {
       best_t = t;
       best_s = s;
