@@ -224,7 +224,10 @@ enum imbd_kernel_class {
 };
 /* Start recording HIP events around every launch of kernel class `cls` whose layer tag
  * equals `layer` (-1: any layer), up to max_launches launches. Creates the events
- * (outside any compute call). Returns IMBD_EINVAL if a recording is already open. */
+ * (outside any compute call). The fused weight-gradient + update kernel takes the
+ * events in its own dispatch (hipExtLaunchKernelGGL), so they hold its start and end
+ * times; other launches get events enqueued before and after them. Returns IMBD_EINVAL
+ * if a recording is already open. */
 int imbd_timing_begin(int cls, int layer, int max_launches);
 /* Stop recording, wait for the recorded events, and return the number of launches and
  * the summed kernel time in milliseconds. Destroys the events. */

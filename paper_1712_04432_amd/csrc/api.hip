@@ -63,19 +63,23 @@ struct Timing {
 } g_timing;
 }  // namespace
 
-LaunchTimer::LaunchTimer(int cls, int layer, hipStream_t s) : stream(s), slot(-1) {
+LaunchTimer::LaunchTimer(int cls, int layer, hipStream_t s, bool in_dispatch_)
+    : stream(s), slot(-1), in_dispatch(in_dispatch_) {
   if (!g_timing.active) return;
   std::lock_guard<std::mutex> lk(g_timing.mu);
   if (!g_timing.active || g_timing.cls != cls || (g_timing.layer >= 0 && g_timing.layer != layer) ||
       g_timing.used >= g_timing.max)
     return;
   slot = g_timing.used++;
-  (void)hipEventRecord(g_timing.ev[2 * slot], s);
+  if (!in_dispatch) (void)hipEventRecord(g_timing.ev[2 * slot], s);
 }
 
 LaunchTimer::~LaunchTimer() {
-  if (slot >= 0) (void)hipEventRecord(g_timing.ev[2 * slot + 1], stream);
+  if (slot >= 0 && !in_dispatch) (void)hipEventRecord(g_timing.ev[2 * slot + 1], stream);
 }
+
+hipEvent_t LaunchTimer::start() const { return slot >= 0 ? g_timing.ev[2 * slot] : nullptr; }
+hipEvent_t LaunchTimer::stop() const { return slot >= 0 ? g_timing.ev[2 * slot + 1] : nullptr; }
 
 // ------------------------------------------------------------------ validation
 static bool valid_dtype(int d) { return d == IMBD_F32 || d == IMBD_BF16; }
@@ -238,14 +242,28 @@ int64_t mlp_workspace_offset(const imbd_mlp_desc *desc, int kind, int layer) {
   }
 }
 
-int mlp_fwd(const imbd_mlp_desc *d, const imbd_layer *layers, const void *x, const int32_t *labels,
-            void *ws, size_t ws_bytes, float *loss, void *stream) {
+}  // extern "C"
+
+namespace imbd {
+// The loss mean of an iteration when it is left to a later launch of the iteration.
+struct LossJob {
+  const float *rows = nullptr;
+  float *loss = nullptr;
+  int n = 0;
+  float scale = 1.0f;
+  bool pending = false;
+};
+}  // namespace imbd
+
+// Forward pass and loss. With job set, the fused top-layer path leaves the loss mean in
+// *job for a later launch instead of launching it.
+static int fwd_impl(const imbd_mlp_desc *d, const imbd_layer *layers, const void *x, const int32_t *labels,
+                    void *ws, size_t ws_bytes, float *loss, hipStream_t s, LossJob *job) {
   MlpLayout lay;
   TRY(mlp_layout(d, &lay));
   TRY(check_layers(d, layers, false));
   if (!x || !labels || !loss) FAIL(IMBD_EINVAL, "x, labels and loss must be set");
   TRY(check_ws(lay, ws, ws_bytes));
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int L = d->n_layers, B = d->batch;
   void *part = at(ws, lay.partial);
   for (int i = 1; i <= L; ++i) {
@@ -269,7 +287,9 @@ int mlp_fwd(const imbd_mlp_desc *d, const imbd_layer *layers, const void *x, con
       if (lay.partial_bytes < gemm_plan(p).ws_bytes) FAIL(IMBD_EWORKSPACE, "partial-sum region too small");
       float *rl = reinterpret_cast<float *>(at(ws, lay.rowloss));
       TRY(run_skinny_softmax(p, part, labels, 1.0f / (float)B, rl, at(ws, lay.dy[L]), d->dims[L], d->dtype, s));
-      return run_loss_mean(B, rl, 1.0f / (float)B, loss, s);
+      if (!job) return run_loss_mean(B, rl, 1.0f / (float)B, loss, s);
+      *job = LossJob{rl, loss, B, 1.0f / (float)B, true};
+      return IMBD_OK;
     }
     TRY(gemm_run(p, part, lay.partial_bytes, s));
   }
@@ -278,15 +298,15 @@ int mlp_fwd(const imbd_mlp_desc *d, const imbd_layer *layers, const void *x, con
                           at(ws, lay.dy[L]), d->dims[L], d->dtype, s, L);
 }
 
-int mlp_bwd(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, void *ws, size_t ws_bytes,
-            int fuse_sgd, float lr, void *dx1, void *stream) {
+// Backward pass. A pending loss mean in *job rides on the top layer's Delta_X launch.
+static int bwd_impl(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, void *ws, size_t ws_bytes,
+                    int fuse_sgd, float lr, void *dx1, hipStream_t s, LossJob *job) {
   MlpLayout lay;
   TRY(mlp_layout(d, &lay));
   TRY(check_layers(d, layers, !fuse_sgd));
   if (!x) FAIL(IMBD_EINVAL, "x must be set");
   if (fuse_sgd && !std::isfinite(lr)) FAIL(IMBD_EINVAL, "lr must be finite");
   TRY(check_ws(lay, ws, ws_bytes));
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int L = d->n_layers;
   void *part = at(ws, lay.partial);
   for (int i = L; i >= 1; --i) {
@@ -309,6 +329,13 @@ int mlp_bwd(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, void *ws,
       }
       e.ldo = d->dims[i - 1];
       e.out_dtype = d->dtype;
+      if (job && job->pending) {
+        p.aux_rows = job->rows;
+        p.aux_loss = job->loss;
+        p.aux_n = job->n;
+        p.aux_scale = job->scale;
+        job->pending = false;
+      }
       TRY(gemm_run(p, part, lay.partial_bytes, s));
     }
     // Delta_W_i with the bias gradient from the same pass (row sums of the Delta_Y tile)
@@ -338,10 +365,31 @@ int mlp_bwd(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, void *ws,
   return IMBD_OK;
 }
 
+extern "C" {
+
+int mlp_fwd(const imbd_mlp_desc *d, const imbd_layer *layers, const void *x, const int32_t *labels,
+            void *ws, size_t ws_bytes, float *loss, void *stream) {
+  return fwd_impl(d, layers, x, labels, ws, ws_bytes, loss, reinterpret_cast<hipStream_t>(stream), nullptr);
+}
+
+int mlp_bwd(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, void *ws, size_t ws_bytes,
+            int fuse_sgd, float lr, void *dx1, void *stream) {
+  return bwd_impl(d, layers, x, ws, ws_bytes, fuse_sgd, lr, dx1, reinterpret_cast<hipStream_t>(stream), nullptr);
+}
+
+// One iteration; the loss mean travels with the top layer's Delta_X launch when both take
+// the skinny path (one launch fewer), else it gets its own launch.
 int mlp_train_step(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, const int32_t *labels,
                    void *ws, size_t ws_bytes, float lr, float *loss, void *stream) {
-  TRY(mlp_fwd(d, layers, x, labels, ws, ws_bytes, loss, stream));
-  return mlp_bwd(d, layers, x, ws, ws_bytes, 1, lr, nullptr, stream);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  LossJob job;
+  TRY(fwd_impl(d, layers, x, labels, ws, ws_bytes, loss, s, &job));
+  const int rc = bwd_impl(d, layers, x, ws, ws_bytes, 1, lr, nullptr, s, &job);
+  if (job.pending) {
+    const int rc2 = run_loss_mean(job.n, job.rows, job.scale, job.loss, s);
+    if (rc == IMBD_OK) return rc2;
+  }
+  return rc;
 }
 
 int sgd_step(float *w, void *w_lp, int lp_dtype, const float *grad, int64_t n, float lr, float grad_scale,

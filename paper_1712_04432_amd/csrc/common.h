@@ -77,6 +77,13 @@ struct GemmProblem {
   float bias_lr = 0.0f;
   int kclass = IMBD_K_GEMM_FWD;  // timing tag
   int layer = 0;
+  // Optional side job enqueued with the product: *aux_loss = aux_scale * sum of the aux_n
+  // values at aux_rows (the batch mean of the per-sample losses, carried by a later launch
+  // of the iteration instead of a launch of its own).
+  const float *aux_rows = nullptr;
+  float *aux_loss = nullptr;
+  int aux_n = 0;
+  float aux_scale = 1.0f;
 };
 
 // Launch plan chosen for a product (a pure function of the shapes).
@@ -135,12 +142,17 @@ size_t conv_wgrad_ws_bytes(int N, int H, int W, int Ci, int Co);
 void set_error(const char *fmt, ...);
 int check_launch(const char *what);
 
-// Records HIP events around one launch when timing is active for (cls, layer).
+// Records HIP events around one launch when timing is active for (cls, layer). With
+// in_dispatch the events are not enqueued around the launch: the launch passes start()
+// and stop() to hipExtLaunchKernelGGL, which stamps the kernel's own start and end.
 struct LaunchTimer {
-  LaunchTimer(int cls, int layer, hipStream_t s);
+  LaunchTimer(int cls, int layer, hipStream_t s, bool in_dispatch = false);
   ~LaunchTimer();
+  hipEvent_t start() const;  // nullptr when this launch is not timed
+  hipEvent_t stop() const;
   hipStream_t stream;
   int slot;
+  bool in_dispatch;
 };
 
 }  // namespace imbd

@@ -18,19 +18,27 @@
 // Each wave keeps its own memory counter, so the groups do not wait on each other's
 // traffic; they meet at one barrier per slab and two per tile (staging free / full).
 
+#include <hip/hip_ext.h>
+
 #include "cdna4.h"
 
 namespace imbd {
 namespace {
 
-// Cache policy of the fp32 master loads: non-temporal. The masters are read once per
-// step; keeping them out of the caches leaves the bf16 copy this kernel writes (which
-// the next step's forward product reads) resident in the 256 MB MALL. In the AlexNet FC
-// step that takes the layer-1 forward from 39 to 29 us and this kernel's layer-1 launch
-// from 82 to 76 us. The master and bf16 stores keep the default policy (non-temporal
-// master stores shortened the step a little further but slowed this kernel).
+// Cache policies (the aux operand of the raw buffer builtins: 2 = nt, 16 = sc1).
+//  * fp32 master loads: non-temporal. The masters are touched once per step; keeping them
+//    out of the caches leaves the bf16 copy this kernel writes (which the next step's
+//    forward product reads) resident in the 256 MB MALL. In the AlexNet FC step that took
+//    the layer-1 forward from 39 to 29 us.
+//  * fp32 master stores: non-temporal and device scope (write-through past the XCD's L2),
+//    for the same reason, and so that the L2s hold no dirty lines for the end-of-kernel
+//    writeback, which otherwise delays the next launch by ~5 us.
+//  * bf16 copy stores: device scope, allocated in the MALL for the next forward.
+// Together the stores take the AlexNet FC step from 245 to 233 us, although the layer-1
+// launch itself runs ~2 us longer than with default stores.
 constexpr int CPOL_MASTER_LD = 2;
-constexpr int CPOL_MASTER_ST = 0;
+constexpr int CPOL_MASTER_ST = 2 | 16;
+constexpr int CPOL_COPY_ST = 16;
 
 struct DwArgs {
   const uint16_t *X;   // [K][ldx]  rows are samples, M = d_in columns
@@ -303,7 +311,7 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
           pk[0] = cvt_pk_bf16(nw[0], nw[1]);
           pk[1] = cvt_pk_bf16(nw[2], nw[3]);
           __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, nw), rp, vp + pp * wrow, 0, CPOL_MASTER_ST);
-          __builtin_amdgcn_raw_buffer_store_b64(pk, rh, vh + pp * hrow, 0, CPOL_MASTER_ST);
+          __builtin_amdgcn_raw_buffer_store_b64(pk, rh, vh + pp * hrow, 0, CPOL_COPY_ST);
         }
         // refill the registers of chunk ch - LAG (tile it) or ch - LAG + CHUNKS (tile it-1)
 #pragma unroll
@@ -368,8 +376,8 @@ int run_dw_sgd(const GemmProblem &p, hipStream_t s) {
   const int tiles = d.tiles_m * d.tiles_n;
   const int grid = tiles < 256 ? tiles : (256 / d.tiles_n) * d.tiles_n;
   {
-    LaunchTimer t(p.kclass, p.layer, s);
-    hipLaunchKernelGGL(dw_sgd_kernel, dim3(grid), dim3(512), 0, s, d);
+    LaunchTimer t(p.kclass, p.layer, s, true);
+    hipExtLaunchKernelGGL(dw_sgd_kernel, dim3(grid), dim3(512), 0, s, t.start(), t.stop(), 0, d);
   }
   return check_launch("dw_sgd");
 }

@@ -918,8 +918,16 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     set_error("bias sums need the B operand stored [k][n]");
     return IMBD_EINVAL;
   }
-  if (p.M <= 0 || p.N <= 0) return IMBD_OK;
   const GemmPlan pl = gemm_plan(p);
+  if (p.aux_loss && (pl.cfg >= 0 || p.M <= 0 || p.N <= 0)) {
+    // only the skinny reduce carries the side job; elsewhere it gets its own launch
+    GemmProblem q = p;
+    q.aux_loss = nullptr;
+    const int rc = gemm_run(q, ws, ws_bytes, s);
+    if (rc != IMBD_OK) return rc;
+    return run_loss_mean(p.aux_n, p.aux_rows, p.aux_scale, p.aux_loss, s);
+  }
+  if (p.M <= 0 || p.N <= 0) return IMBD_OK;
   if (pl.ws_bytes > 0 && (ws == nullptr || ws_bytes < pl.ws_bytes)) {
     set_error("product %dx%dx%d needs %zu bytes of workspace for split-K partials, got %zu",
               p.M, p.N, p.K, pl.ws_bytes, ws_bytes);

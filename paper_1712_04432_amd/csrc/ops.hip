@@ -4,6 +4,7 @@
 // so repeated calls give identical bits.
 
 #include "common.h"
+#include "loss_mean.h"
 
 namespace imbd {
 
@@ -82,20 +83,11 @@ __global__ void __launch_bounds__(256)
   }
 }
 
-// loss = inv_batch * sum_b row_loss[b], one workgroup, fixed order: each thread sums a
-// strided subset in ascending order, then a fixed tree over the threads.
+// loss = inv_batch * sum_b row_loss[b], one workgroup (the fixed order of block_loss_mean).
 __global__ void __launch_bounds__(256)
     loss_mean(int B, const float *__restrict__ row_loss, float inv_batch, float *__restrict__ loss) {
   __shared__ float part[256];
-  float s = 0.f;
-  for (int b = threadIdx.x; b < B; b += 256) s += row_loss[b];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) *loss = inv_batch * part[0];
+  block_loss_mean(B, row_loss, inv_batch, loss, part);
 }
 
 // db[m] = alpha * sum_b dy[b][m]: 64 columns per workgroup, each column's rows split in

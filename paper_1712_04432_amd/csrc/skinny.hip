@@ -23,6 +23,7 @@
 #include <stdlib.h>
 
 #include "cdna4.h"
+#include "loss_mean.h"
 
 namespace imbd {
 namespace {
@@ -243,7 +244,8 @@ __global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
   lds_barrier();
   // ---- partial tile out: one contiguous block, 16 threads per 256-byte row. Device-scope
   // stores (sc1) write through the XCD's L2, so the partials do not sit there dirty until
-  // the end-of-kernel writeback (measured 1-2 us faster per product than default stores).
+  // the end-of-kernel writeback (the AlexNet FC step is ~6 us faster than with default
+  // stores).
   const float *stg = reinterpret_cast<const float *>(smem);
   float *dst = a.partial + (int64_t)split * a.sstride + (int64_t)(m0 / SK_BM) * a.tpitch;
   const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(dst, 0, (int)(a.tpitch * 4), BUF_DW3);
@@ -263,6 +265,10 @@ struct SkReduceArgs {
   int64_t tpitch, sstride;
   int M, N, splits;
   Epilogue epi;
+  const float *aux_rows;  // side job in one extra workgroup: *aux_loss = aux_scale * sum
+  float *aux_loss;
+  int aux_n;
+  float aux_scale;
 };
 
 // Adds the splits' partials in split order (the same order and arithmetic as the
@@ -271,6 +277,11 @@ struct SkReduceArgs {
 // sample per thread; VEC: every access is whole and aligned (checked on the host).
 template <bool VEC>
 __global__ void __launch_bounds__(256) skinny_reduce(SkReduceArgs g) {
+  if (g.aux_loss && blockIdx.x == gridDim.x - 1) {
+    __shared__ float part[256];
+    block_loss_mean(g.aux_n, g.aux_rows, g.aux_scale, g.aux_loss, part);
+    return;
+  }
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int tile = (int)(t / ((int64_t)g.N * 8));
   const int r = (int)(t - (int64_t)tile * g.N * 8);
@@ -426,16 +437,17 @@ bool skinny_fits(const GemmProblem &p) {
          ((int64_t)256 * p.ldb + p.K + SK_KS) * 2 < ((int64_t)1 << 31) && (p.a_kc || p.M % 8 == 0);
 }
 
-// Splits: fill the chip, traded against the partials (each split writes an fp32 M x N
-// partial, which the reduce reads back). Modelled time of a split count: the larger of
-// the HBM time of the operands and the time of one workgroup (~0.5 us per slab plus ~3 us
-// of fill and write-out) times the rounds of workgroups over 256 CUs, plus ~1 us per MB
-// of partials for writing them out and reading them back (fitted to timings of the
-// AlexNet FC products at B = 256: more, shorter workgroups lose once the partials grow,
-// e.g. the 1000 x 4096 forward is fastest at 6 splits on 96 workgroups).
+// Splits: fill the chip, traded against the partials' traffic (each split writes an
+// fp32 M x N partial, which the reduce reads back). Modelled time of a split count: the
+// larger of the HBM time (W, the activations once, the partials written and read) and
+// the time of one workgroup (slabs at ~900 cycles each plus ~12k cycles of fill and
+// partial write-out), times the rounds of workgroups over 256 CUs. (Timed alone, several
+// products run faster on fewer workgroups with fewer splits, e.g. the 1000 x 4096
+// forward on 5 splits instead of 13; inside the training step those plans lose ~7 us,
+// so the model keeps the chip full.)
 void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
   const int tiles = (p.M + SK_BM - 1) / SK_BM;
-  const double hbm = 5.0e12, clk = 2.1e9, slab_clk = 1050.0, fill_clk = 6300.0, part_bw = 1.0e12;
+  const double hbm = 5.0e12, clk = 2.1e9, slab_clk = 900.0, fill_clk = 12000.0;
   int best_s = 1;
   double best_t = 1e30;
   const int forced = env_splits();
@@ -444,11 +456,10 @@ void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
     if ((p.K + ks - 1) / ks != s) continue;
     const int blocks = tiles * s;
     if (blocks > 65535) break;
-    const double bytes = 2.0 * p.M * p.K + 2.0 * p.N * p.K;
-    const double part = 4.0 * s * (double)tiles * SK_BM * p.N;
+    const double bytes = 2.0 * p.M * p.K + 2.0 * p.N * p.K + 8.0 * s * (double)p.M * p.N;
     const int rounds = (blocks + 255) / 256;
     const double t_cu = rounds * ((ks / SK_KS) * slab_clk + fill_clk) / clk;
-    const double t = (bytes / hbm > t_cu ? bytes / hbm : t_cu) + part / part_bw;
+    const double t = bytes / hbm > t_cu ? bytes / hbm : t_cu;
     if (forced > 0 ? s == forced : t < best_t * 0.98) {
       best_t = t;
       best_s = s;
@@ -508,12 +519,16 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
   r.N = p.N;
   r.splits = splits;
   r.epi = p.epi;
+  r.aux_rows = p.aux_rows;
+  r.aux_loss = p.aux_n > 0 ? p.aux_loss : nullptr;
+  r.aux_n = p.aux_n;
+  r.aux_scale = p.aux_scale;
   const Epilogue &e = p.epi;
   auto al = [](const void *q, int a) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const bool vec = p.M % 8 == 0 && al(e.out, 16) && e.ldo % 8 == 0 &&
                    (e.mask == nullptr || (al(e.mask, 16) && e.ldmask % 8 == 0));
   const int64_t threads = (int64_t)g.tiles_m * p.N * 8;
-  const unsigned blocks = (unsigned)((threads + 255) / 256);
+  const unsigned blocks = (unsigned)((threads + 255) / 256) + (r.aux_loss ? 1u : 0u);
   {
     LaunchTimer t(IMBD_K_SPLITK, p.layer, s);
     if (vec) hipLaunchKernelGGL(skinny_reduce<true>, dim3(blocks), dim3(256), 0, s, r);

@@ -155,6 +155,28 @@ def test_bf16_ten_steps_match_mirrored_oracle(imbd, dev):
     assert nrm_err(losses_g, losses_o) < TOL_BF16
 
 
+@pytest.mark.parametrize("dims,B", [((576, 320, 256, 100), 64), ((64, 32, 10), 16), ((256, 100), 32)])
+def test_train_step_loss_equals_forward_loss(imbd, dev, dims, B):
+    """mlp_train_step computes the loss mean inside a later launch of the iteration (the
+    top layer's Delta_X reduce) when it can, else in a launch of its own (a Delta_X
+    product off the skinny path; a one-layer network, which has no Delta_X product):
+    every route gives the bits of mlp_fwd's loss, and the oracle's loss."""
+    import torch
+    cfg = scaled_mlp(dims, B, "bf16")
+    _flush(f"train-step loss {dims} B={B}")
+    d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev, seed=6)
+    imbd.mlp_fwd(net, layers, x, lab, ws, loss)
+    torch.cuda.synchronize()
+    fwd_loss = loss.clone()
+    d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev, seed=6)
+    loss.fill_(float("nan"))
+    imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
+    torch.cuda.synchronize()
+    assert torch.equal(loss, fwd_loss)
+    ref = oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, "bf16")
+    assert abs(loss.item() - ref["loss"]) < TOL_BF16 * abs(ref["loss"])
+
+
 def test_step_is_deterministic(imbd, dev):
     import torch
     cfg = scaled_mlp((2048, 512, 256, 100), 128, "bf16")
