@@ -202,26 +202,56 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
     for (int s = 0; s < NS; ++s) issue();
     vm_barrier<(NS - 1) * DMA_PER_SLAB>();  // Delta_Y block and slab 0 landed
 
-    // Bias gradient: the column sums of Delta_Y, once, by the workgroups whose first tile
-    // is in the first row block. Lanes l and l+32 of a wave split the batch of one column.
-    if (a.db_mode != 0 && b < tiles && grp == 0) {
-      const int c = wave * 32 + (lane & 31), half = lane >> 5;
-      const int kh = (KMAX / 2);
-      float sum = 0.f;
-      for (int r = half * kh; r < half * kh + kh; ++r) {
+    // Bias gradient: the column sums of the resident Delta_Y block, once per column block,
+    // by the workgroup with index 0 in the block's group (it always has a tile). Wave w
+    // sums rows 64w..64w+63: lane l reads 16-byte chunk l%16 (columns 8(l%16)..+7) of rows
+    // 64w + l/16 + 4i, i < 16, and the four row phases are added across lanes. The waves'
+    // sums go to the staging buffer (unused until the first tile is handed off) and wave 0
+    // adds them in wave order after the next slab barrier, which every wave reaches only
+    // after writing its sums.
+    bool bias_pending = a.db_mode != 0 && b < tiles && grp == 0;
+    if (bias_pending) {
+      const int j = lane & 15, q = lane >> 4;
+      float cs[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) cs[e] = 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = 64 * wave + q + 4 * i;
         const int sw = 2 * (r & 3) + 8 * ((r >> 3) & 1);
-        const uint16_t v = *(const __attribute__((address_space(3))) uint16_t *)(uintptr_t)(
-            ldy + (uint32_t)(r * ROWB + (((c >> 3) ^ sw) << 4) + 2 * (c & 7)));
-        sum += bf16_to_f32(v);
+        const u32x4 v = *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(ldy + (uint32_t)(r * ROWB + ((j ^ sw) << 4)));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          cs[2 * e] += bf16_to_f32((uint16_t)(v[e] & 0xffffu));
+          cs[2 * e + 1] += bf16_to_f32((uint16_t)(v[e] >> 16));
+        }
       }
-      sum += __shfl_xor(sum, 32, 64);
-      const int n = n0 + c;
-      if (half == 0 && n < a.N) {
-        const float g = a.db_alpha * sum;
-        if (a.db_mode == 1) a.db_out[n] = g;
-        else a.bias[n] = fmaf(-a.bias_lr, g, a.bias[n]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        cs[e] += __shfl_xor(cs[e], 16, 64);
+        cs[e] += __shfl_xor(cs[e], 32, 64);
+      }
+      if (q == 0) {
+        float *dst = stg + wave * BN + 8 * j;
+        *reinterpret_cast<f32x4 *>(dst) = f32x4{cs[0], cs[1], cs[2], cs[3]};
+        *reinterpret_cast<f32x4 *>(dst + 4) = f32x4{cs[4], cs[5], cs[6], cs[7]};
       }
     }
+    auto bias_finish = [&]() {
+      if (wave == 0) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int c = lane + 64 * h, n = n0 + c;
+          const float sum = stg[c] + stg[BN + c] + stg[2 * BN + c] + stg[3 * BN + c];
+          if (n < a.N) {
+            const float g = a.db_alpha * sum;
+            if (a.db_mode == 1) a.db_out[n] = g;
+            else a.bias[n] = fmaf(-a.bias_lr, g, a.bias[n]);
+          }
+        }
+      }
+      bias_pending = false;
+    };
 
     int c_ks = 0;
     uint32_t c_slot = 0, c_krow = 0;
@@ -231,6 +261,7 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
       // Slab s+1 landed once at most the later NS-2 slabs' loads are outstanding; every
       // wave has read slab s, so its slot takes the next slab in line.
       vm_barrier<(NS - 2) * DMA_PER_SLAB>();
+      if (bias_pending) bias_finish();  // before any handoff can reuse the staging buffer
       issue();
       c_slot = c_slot + XSLAB == NS * XSLAB ? 0u : c_slot + XSLAB;
       const bool tile_end = ++c_ks == TK;
