@@ -11,7 +11,8 @@ weight-gradient kernel with the fused update, timed with HIP events inside the t
 region's twin) and the CPU oracle timed on a bounded sample of the same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
-(--workload conv3x3_tile measures the domain-parallel conv tile instead of the FC step)
+(--workload conv3x3_tile measures the domain-parallel conv tile instead of the FC step;
+--workload batch_sweep times the FC step at batch sizes 1..2048, --stack alexnet|vgg)
 """
 from __future__ import annotations
 
@@ -183,6 +184,88 @@ def bench_conv(args):
     print(json.dumps(result), flush=True)
 
 
+def step_hbm_bytes(dims, batch: int) -> int:
+    """Algorithmic HBM bytes of one fused SGD iteration of a bf16 FC stack: per layer the
+    bf16 weights read by the forward and Delta_X products, the fp32 master read and written
+    and the bf16 copy written by the fused update (10 B per weight), and the activations,
+    gradients and logits read or written once per product."""
+    total = 0
+    L = len(dims) - 1
+    for i in range(1, L + 1):
+        din, dout = dims[i - 1], dims[i]
+        w = din * dout
+        total += 2 * w + 2 * batch * (din + dout)                       # forward
+        if i >= 2:
+            total += 2 * w + 2 * batch * dout + 4 * batch * din         # Delta_X (+ mask)
+        total += 10 * w + 2 * batch * (din + dout)                      # Delta_W + update
+    total += 8 * batch * dims[L]                                        # logits, softmax
+    return total
+
+
+def bench_batch_sweep(args):
+    """Step time of the FC stack against the batch size (the single-GPU analogue of the
+    paper's per-batch timing of the forward and backward passes): one fixed synthetic batch
+    per size, the weights shared, fused SGD as in the default workload."""
+    import numpy as np
+    import torch
+
+    import paper_1712_04432_amd as m
+    from synthdata import get_config, make_mlp_inputs, scaled_mlp
+
+    m.load()
+    base = get_config("alexnet_fc_b256" if args.stack == "alexnet" else "vgg_fc_b512")
+    dev = torch.device("cuda:0")
+    batches = [int(b) for b in args.batches.split(",")]
+    d = make_mlp_inputs(base, seed=0, batch=1)
+    w32 = [torch.from_numpy(w).to(dev) for w in d["w"]]
+    rows = []
+    for B in batches:
+        cfg = scaled_mlp(base.dims, B, "bf16", x_dist=base.x_dist, name=f"{base.name.split('_b')[0]}_b{B}")
+        db = make_mlp_inputs(cfg, seed=1, batch=B)
+        net = m.MLP(cfg.dims, B, "bf16")
+        layers = []
+        for w, b in zip(w32, db["b"]):
+            wm = w.clone()
+            wlp = torch.empty(w.shape, dtype=torch.bfloat16, device=dev)
+            m.cast_f32_bf16(wm, wlp)
+            layers.append({"w": wm, "w_lp": wlp, "b": torch.from_numpy(b).to(dev)})
+        x = torch.from_numpy(db["x_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+        lab = torch.from_numpy(db["labels"]).to(dev)
+        ws = torch.zeros(m.mlp_workspace_bytes(net), dtype=torch.uint8, device=dev)
+        loss = torch.zeros(1, device=dev)
+        stream = torch.cuda.current_stream()
+        for _ in range(args.warmup):
+            m.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss, stream=stream)
+        torch.cuda.synchronize()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for _ in range(args.steps):
+            m.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss, stream=stream)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop) / args.steps
+        flops = cfg.gemm_flops()
+        hbm = step_hbm_bytes(cfg.dims, B)
+        t_hbm_ms = hbm / (PEAK_HBM_GBS * 1e9) * 1e3
+        t_mfma_ms = flops / (PEAK_BF16_TFLOPS * 1e12) * 1e3
+        rows.append({"batch": B, "ms_per_step": round(ms, 5), "tflops": round(flops / (ms * 1e-3) / 1e12, 3),
+                     "samples_per_s": round(B / (ms * 1e-3), 1),
+                     "pct_bf16_mfma_peak": round(100.0 * flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 3),
+                     "roofline_ms": round(max(t_hbm_ms, t_mfma_ms), 5),
+                     "roofline_bound": "hbm" if t_hbm_ms >= t_mfma_ms else "mfma",
+                     "frac_of_roofline": round(max(t_hbm_ms, t_mfma_ms) / ms, 4),
+                     "loss": round(loss.item(), 5)})
+        log(f"bench: B={B} {ms * 1e3:.1f} us/step, {rows[-1]['tflops']} TFLOP/s")
+        del layers, x, lab, ws, net
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "FC step time and TFLOP/s against the batch size", "unit": "TFLOP/s",
+                      "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
+                      "data": "synthetic (seeded inputs and labels per batch size, He-initialised weights)",
+                      "config": {"workload": f"batch_sweep: {'-'.join(map(str, base.dims))} FC stack, fused SGD",
+                                 "parallelism": "single GPU"},
+                      "sweep": rows}), flush=True)
+
+
 def bench_copy(args):
     """A plain device-to-device copy of 512 MiB: the calibration run for the HBM byte
     counters (FETCH_SIZE / WRITE_SIZE per dispatch against the known 512 MiB each way)
@@ -215,6 +298,8 @@ def main():
     ap.add_argument("--workload", default="alexnet_fc_b256")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-batch", type=int, default=8)
+    ap.add_argument("--stack", default="alexnet", choices=("alexnet", "vgg"))
+    ap.add_argument("--batches", default="1,2,4,8,16,32,64,128,256,512,1024,2048")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
@@ -225,6 +310,8 @@ def main():
         return bench_conv(args)
     if args.workload == "hbm_copy":
         return bench_copy(args)
+    if args.workload == "batch_sweep":
+        return bench_batch_sweep(args)
 
     import numpy as np
     import torch

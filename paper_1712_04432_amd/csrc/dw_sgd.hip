@@ -374,7 +374,7 @@ bool dw_sgd_fits(const GemmProblem &p) {
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   return p.dtype == IMBD_BF16 && !p.a_kc && !p.b_kc && e.mode == EPI_SGD && e.out2 && !e.mask && !e.bias &&
          !e.relu && p.K > 0 && p.K <= 256 && p.M > 0 && p.N > 0 && p.N <= 256 * 128 && p.M % 8 == 0 &&
-         p.N % 8 == 0 && p.K % 8 == 0 && al(p.A, 16) && al(p.B, 16) && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+         p.N % 8 == 0 && al(p.A, 16) && al(p.B, 16) && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
          al(e.out, 16) && e.ldo % 4 == 0 && al(e.out2, 8) && e.ldo2 % 4 == 0 && e.ldo < (1 << 21) &&
          e.ldo2 < (1 << 21) && (int64_t)p.K * p.lda * 2 < ((int64_t)1 << 31) &&
          (int64_t)p.K * p.ldb * 2 < ((int64_t)1 << 31);

@@ -98,7 +98,8 @@ def test_bf16_one_step_matches_mirrored_oracle(imbd, dev, dims, B):
         assert nrm_err(host(layers[i]["db"]), ref["db"][i]) < TOL_BF16, i
 
 
-@pytest.mark.parametrize("dims,B", [((2056, 2104, 24), 72), ((136, 8, 16), 8), ((4096, 1000, 128), 256)])
+@pytest.mark.parametrize("dims,B", [((2056, 2104, 24), 72), ((136, 8, 16), 8), ((4096, 1000, 128), 256),
+                                    ((136, 8, 16), 1), ((264, 128, 24), 5)])
 def test_bf16_fused_update_matches_oracle(imbd, dev, dims, B):
     """The fused weight update (Eq. (1) applied inside the weight-gradient product) on
     shapes that give the persistent update kernel several tiles per workgroup (17 x 17
@@ -193,15 +194,16 @@ def test_step_is_deterministic(imbd, dev):
 # ------------------------------------------------------------------ full-size stacks
 def _sampled_full_step(imbd, dev, name, n_rows=24, n_cols=32, seed=0):
     """One fused step at full size; per layer, sampled outputs recomputed by the oracle from
-    the device's own inputs to that layer (bf16 bits read back)."""
+    the device's own inputs to that layer (bf16 bits read back). name: a configuration
+    name or a configuration."""
     import torch
-    cfg = get_config(name)
-    _flush(f"full step {name}")
+    cfg = get_config(name) if isinstance(name, str) else name
+    _flush(f"full step {cfg.name} B={cfg.batch}")
     d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev, seed=seed)
     L = cfg.n_layers
     B = cfg.batch
     rng = np.random.default_rng(99)
-    rows = [rng.choice(B, n_rows, replace=False) for _ in range(L + 1)]
+    rows = [rng.choice(B, min(n_rows, B), replace=False) for _ in range(L + 1)]
     cols = [None] + [np.sort(rng.choice(cfg.dims[i], min(n_cols, cfg.dims[i]), replace=False))
                      for i in range(1, L + 1)]
     ci = [None] + [torch.from_numpy(c).to(dev) for c in cols[1:]]
@@ -249,6 +251,15 @@ def test_alexnet_fc_b256_full_size_sampled(imbd, dev):
 
 def test_vgg_fc_b512_full_size_sampled(imbd, dev):
     _sampled_full_step(imbd, dev, "vgg_fc_b512", n_rows=16, n_cols=16)
+
+
+@pytest.mark.parametrize("B", [1, 8, 100, 257, 1024, 2048])
+def test_alexnet_fc_batch_sweep_sizes_sampled(imbd, dev, B):
+    """The batch sizes of the batch sweep (bench.py --workload batch_sweep) beyond the
+    benchmark's 256: one sample (B = 1), ragged batches on the skinny path (100) and past
+    it (257), and the large batches on the tiled products (1024, 2048)."""
+    cfg = scaled_mlp((9216, 4096, 4096, 1000), B, "bf16", name="alexnet_fc")
+    _sampled_full_step(imbd, dev, cfg, n_rows=16, n_cols=16)
 
 
 def test_workspace_too_small_on_device(imbd, dev):
