@@ -12,7 +12,9 @@ region's twin) and the CPU oracle timed on a bounded sample of the same workload
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 (--workload conv3x3_tile measures the domain-parallel conv tile instead of the FC step;
---workload batch_sweep times the FC step at batch sizes 1..2048, --stack alexnet|vgg)
+--workload batch_sweep times the FC step at batch sizes 1..2048, --stack alexnet|vgg;
+--workload grid_model times one process's local blocks of the FC stack for every P_r x P_c
+grid of --procs and picks the grid with the cost model of paper_1712_04432_amd.gridmodel)
 """
 from __future__ import annotations
 
@@ -266,6 +268,94 @@ def bench_batch_sweep(args):
                       "sweep": rows}), flush=True)
 
 
+# Collective parameters for the grid model (assumptions, not measured: one GPU here).
+# xGMI inside an 8-GPU node: ~2 us per message, ring all-reduce bus bandwidth ~300 GB/s;
+# between nodes: ~5 us, ~50 GB/s per GPU (8 x 400 Gb/s NICs per node); the paper's Cori
+# simulation: 2 us, 6 GB/s.
+NETWORKS = {"xgmi_node": (2e-6, 1 / 300e9), "multi_node": (5e-6, 1 / 50e9), "paper_cori": (2e-6, 1 / 6e9)}
+
+
+def bench_grid_model(args):
+    """Per-process compute of the 1.5D layout measured on the device (local forward, local
+    backward with the Delta_W and Delta_X partials, SGD of the process's weight block, bf16
+    blocks of the FC stack as the grid cuts them, the largest block when the cut is uneven)
+    and the grid each network's collective parameters select (Sec. 2.3 cost + compute)."""
+    import torch
+
+    import paper_1712_04432_amd as m
+    from paper_1712_04432_amd import gridmodel as gm
+    from synthdata import get_config
+
+    m.load()
+    base = get_config("alexnet_fc_b256" if args.stack == "alexnet" else "vgg_fc_b512")
+    dims, B = base.dims, args.grid_batch
+    layers = [gm.FC(dims[i - 1], dims[i]) for i in range(1, len(dims))]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    cache = {}
+
+    def time_layer(d_out, d_in, b, first):
+        key = (d_out, d_in, b, first)
+        if key in cache:
+            return cache[key]
+        g = torch.Generator(device=dev).manual_seed(0)
+        w = (torch.randn(d_out, d_in, device=dev, generator=g) * 0.01)
+        wl = w.to(torch.bfloat16)
+        x = torch.randn(b, d_in, device=dev, generator=g).relu().to(torch.bfloat16)
+        y = torch.empty(b, d_out, dtype=torch.bfloat16, device=dev)
+        dy = (torch.randn(b, d_out, device=dev, generator=g) * 0.01).to(torch.bfloat16)
+        dw = torch.empty(d_out, d_in, device=dev)
+        db = torch.empty(d_out, device=dev)
+        bias = torch.zeros(d_out, device=dev)
+        dx = None if first else torch.empty(b, d_in, device=dev)
+        wsz = max(m.mlp_local_workspace_bytes(0, m.IMBD_BF16, d_out, d_in, b),
+                  m.mlp_local_workspace_bytes(1, m.IMBD_BF16, d_out, d_in, b), 16)
+        ws = torch.zeros(wsz, dtype=torch.uint8, device=dev)
+
+        def run():
+            m.mlp_local_fwd(wl, x, y, 1, 1, bias=bias, relu=True, ws=ws, stream=stream)
+            m.mlp_local_bwd(wl, dy, x, dw, 1, 1, db_part=db, dx_part=dx, mask_relu=not first, ws=ws,
+                            stream=stream)
+            m.sgd_step(w, dw, 0.01, 1.0 / B, w_lp=wl, stream=stream)
+        for _ in range(2):
+            run()
+        torch.cuda.synchronize()
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        for _ in range(args.steps):
+            run()
+        s1.record(stream)
+        torch.cuda.synchronize()
+        cache[key] = s0.elapsed_time(s1) / args.steps * 1e-3
+        return cache[key]
+
+    def t_comp(P_r, P_c):
+        b = -(-B // P_c)
+        return sum(time_layer(-(-l.d_out // P_r), l.d_in, b, i == 0) for i, l in enumerate(layers))
+
+    procs = [int(p) for p in args.procs.split(",")]
+    out = {"metric": "1.5D grid choice for the FC stack: modelled time per iteration (s)", "n_gpus": 1,
+           "config": {"workload": f"grid_model: {'-'.join(map(str, dims))} FC stack, B = {B}, bf16 local blocks",
+                      "networks": {k: {"alpha_s": a, "bandwidth_GBs": round(1 / b / 1e9, 1)}
+                                   for k, (a, b) in NETWORKS.items()}},
+           "grids": []}
+    for P in procs:
+        comp = {(r, P // r): t_comp(r, P // r) for r, _ in gm.grids(P)}
+        entry = {"P": P, "comp_s": {f"{r}x{c}": round(v, 7) for (r, c), v in comp.items()}, "choice": {}}
+        for name, (a, bt) in NETWORKS.items():
+            best, rows = gm.select_grid(layers, B, P, a, bt, elem_bytes=4, t_comp=lambda r, c: comp[(r, c)],
+                                        divisible=False)
+            pure = [r for r in rows if r["P_r"] == 1][0]
+            bestrow = [r for r in rows if (r["P_r"], r["P_c"]) == best][0]
+            entry["choice"][name] = {"grid": f"{best[0]}x{best[1]}", "total_s": round(bestrow["total"], 7),
+                                     "comm_s": round(bestrow["comm"], 7),
+                                     "batch_grid_total_s": round(pure["total"], 7),
+                                     "speedup_over_batch": round(pure["total"] / bestrow["total"], 3)}
+        log(f"bench: P={P} " + " ".join(f"{k}:{v['grid']}" for k, v in entry["choice"].items()))
+        out["grids"].append(entry)
+    print(json.dumps(out), flush=True)
+
+
 def bench_copy(args):
     """A plain device-to-device copy of 512 MiB: the calibration run for the HBM byte
     counters (FETCH_SIZE / WRITE_SIZE per dispatch against the known 512 MiB each way)
@@ -300,6 +390,8 @@ def main():
     ap.add_argument("--cpu-sample-batch", type=int, default=8)
     ap.add_argument("--stack", default="alexnet", choices=("alexnet", "vgg"))
     ap.add_argument("--batches", default="1,2,4,8,16,32,64,128,256,512,1024,2048")
+    ap.add_argument("--procs", default="8,64,512")
+    ap.add_argument("--grid-batch", type=int, default=2048)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
@@ -312,6 +404,8 @@ def main():
         return bench_copy(args)
     if args.workload == "batch_sweep":
         return bench_batch_sweep(args)
+    if args.workload == "grid_model":
+        return bench_grid_model(args)
 
     import numpy as np
     import torch
