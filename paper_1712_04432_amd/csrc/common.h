@@ -137,6 +137,11 @@ int run_conv_dgrad(int N, int H, int W, int Ci, int Co, const void *dyp, const v
 int run_conv_wgrad(int N, int H, int W, int Ci, int Co, const void *xp, const void *dyp,
                    float *dw, void *ws, size_t ws_bytes, hipStream_t s);
 size_t conv_wgrad_ws_bytes(int N, int H, int W, int Ci, int Co);
+// The forward (pass 1) and input-gradient (pass 2) passes for 256 output channels on the
+// large-tile implicit-GEMM kernel: whether it takes the problem, and the launch.
+bool conv_nt_fits(int pass, int N, int H, int W, int Ci, int Co, const void *act, const void *w, const void *out);
+int run_conv_nt(int pass, int N, int H, int W, int Ci, int Co, const void *act, const void *w, void *out,
+                int out_dtype, hipStream_t s);
 
 // --------------------------------------------------------------------- host helpers
 void set_error(const char *fmt, ...);

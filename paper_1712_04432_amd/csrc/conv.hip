@@ -1,4 +1,318 @@
-// The 3x3 convolution tile's kernels are instantiations of the GEMM template in gemm.hip
-// (implicit GEMM over the padded grid); see run_conv_* there. This file is kept for the
-// conv-specific host declarations only.
-#include "common.h"
+// Forward and input-gradient passes of the domain-parallel 3x3 conv tile (Sec. 2.2, pure
+// domain parallelism: each process convolves its spatial tile with the halo supplied;
+// the input gradient takes the output gradient with its own halo), for 256 output
+// channels, as implicit GEMMs on the zero-padded (H+2) x (W+2) grid:
+//   forward   D(P, o) = sum_{tap, c} x_pad[P + r*(W+2) + s][c] * W[o][tap][c]
+//   input grad D(P, c) = sum_{tap, o} dy_pad[P + (2-r)*(W+2) + 2-s][o] * W[o][tap][c]
+// with tap = 3r + s and P a position of the padded grid; D(P, .) is the output at the
+// interior position of P when P's row and column are inside the tile, and is dropped
+// otherwise. Each tap is a row shift of a dense [positions][channels] matrix, so a k-slab
+// (64 channels of one tap) of the activation operand is 64 contiguous channels of shifted
+// rows.
+//
+// The products are MFMA-bound (2 x 9 x C flops per output), so a workgroup owns a large
+// tile: 128 positions x all 256 channels over the whole K = 9 C (no split, no partials;
+// the epilogue writes the outputs). The kernel keeps the layout of the skinny-batch kernel
+// (csrc/skinny.hip): both operands travel through LDS in 64-k slabs written by buffer
+// loads that go straight to LDS in whole 128-byte lines, loader waves with their own
+// memory counters, one barrier per slab, XOR-swizzled 16-byte chunks:
+//  * waves 4-5 stream the activation slab (128 shifted rows x 128 B) through a 4-slot ring;
+//  * waves 6-7 stream the weight slab (256 channels x 64 k) through a 3-slot ring: rows of
+//    W for the forward pass, k-rows of W (64 output channels of one tap x 256 input
+//    channels, as four 64-channel quarters) for the input gradient, whose fragments then
+//    come from the gfx950 LDS transpose read;
+//  * waves 0-3 each accumulate 128 positions x 64 channels in registers.
+// After the last slab the tile goes through LDS ([position][channel], fp32) and is written
+// as whole 512-byte (bf16) or 1 KB (fp32) rows of the interior positions.
+
+#include <stdlib.h>
+
+#include "cdna4.h"
+
+namespace imbd {
+namespace {
+
+constexpr int CV_BM = 128;             // positions per workgroup
+constexpr int CV_BN = 256;             // channels of the output per workgroup
+constexpr int CV_KS = 64;              // k per slab: 64 channels of one tap
+constexpr int CV_NA = 4;               // activation ring slots
+constexpr int CV_NW = 3;               // weight ring slots
+constexpr int CV_ASLOT = CV_BM * 128;  // 16 KB
+constexpr int CV_WSLOT = CV_BN * 128;  // 32 KB
+constexpr int CV_QSLOT = 64 * 128;     // one 64-channel quarter of a transposed weight slab
+constexpr int CV_PITCH = CV_BN + 4;    // staging row pitch in floats (1040 B)
+
+struct CvArgs {
+  const uint16_t *act;  // x_pad (forward) or dy_pad (input gradient): [N][H+2][W+2][Ck]
+  const uint16_t *w;    // [C_out][3][3][C_in]
+  void *out;            // [N][H][W][256]
+  int out_bf16;
+  int H, W, Ck, Cw;     // Ck: channels of act (the reduction); Cw: C_in (the W row's channel stride)
+  int M, tiles;         // positions computed (up to the last interior one), tiles of 128
+};
+
+__device__ __forceinline__ int cv_swz_kc(int r) { return r & 7; }
+__device__ __forceinline__ int cv_swz_tr(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
+
+// TR: input gradient (W read transposed); else forward.
+template <bool TR>
+__global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int WRING = CV_NW * CV_WSLOT, ARING = CV_NA * CV_ASLOT;
+  __shared__ __attribute__((aligned(1024))) char smem[WRING + ARING];
+  static_assert(WRING + ARING <= 160 * 1024, "LDS");
+  static_assert(CV_BM * CV_PITCH * 4 <= WRING + ARING, "staging");
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // the grid is padded to a multiple of 8; consecutive tiles (which share shifted
+  // activation rows) run on one XCD
+  const int G = gridDim.x;
+  const int b = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+  if (b >= a.tiles) return;
+  const int m0 = b * CV_BM;
+  const int Wp = a.W + 2;
+  const int nsl = 9 * a.Ck / CV_KS;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
+  const uint32_t ldsw = lds0, ldsa = lds0 + WRING;
+  // tap and channel offset of slab S
+  auto tap_of = [&](int S, int C, int *c0) {
+    const int k0 = S * CV_KS;
+    const int t = k0 / C;
+    *c0 = k0 - t * C;
+    return t;
+  };
+
+  if (wave >= 6) {
+    // ------------------------------------------------------- weight loaders (6, 7)
+    const int ww = wave - 6;
+    const i32x4 rw = buf_rsrc(a.w, (uint32_t)((int64_t)9 * a.Ck * CV_BN * 2));
+    uint32_t base[16];
+    uint32_t dst[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int blk = 16 * ww + q;  // 1 KB block of the slot
+      if constexpr (!TR) {
+        // W row o = 8 blk + lane/8, 16-byte chunk (lane%8) ^ swz
+        const int r = 8 * blk + (lane >> 3);
+        const int c = (lane & 7) ^ cv_swz_kc(r);
+        base[q] = (uint32_t)(((int64_t)r * 9 * a.Ck + 8 * c) * 2);
+        dst[q] = (uint32_t)(blk * 1024);
+      } else {
+        // quarter h (input channels 64h..64h+63), k-row (output channel) r of the slab
+        const int h = blk >> 3, g = blk & 7;
+        const int r = 8 * g + (lane >> 3);
+        const int c = (lane & 7) ^ cv_swz_tr(r);
+        base[q] = (uint32_t)(((int64_t)r * 9 * a.Cw + 64 * h + 8 * c) * 2);
+        dst[q] = (uint32_t)(h * CV_QSLOT + g * 1024);
+      }
+    }
+    auto issue = [&](int S) {
+      const uint32_t slot = ldsw + (uint32_t)((S % CV_NW) * CV_WSLOT);
+      uint32_t off = OOB;
+      if (S < nsl) {
+        if constexpr (!TR) {
+          off = (uint32_t)(S * CV_KS * 2);
+        } else {
+          int o0;
+          const int t = tap_of(S, a.Ck, &o0);
+          off = (uint32_t)(((int64_t)o0 * 9 + t) * a.Cw * 2);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 16; ++q) dma16(rw, off == OOB ? OOB : base[q] + off, slot + dst[q]);
+    };
+#pragma unroll
+    for (int S = 0; S < CV_NW - 1; ++S) issue(S);
+    for (int S = 0; S < nsl; ++S) {
+      vm_barrier<16 * (CV_NW - 2)>();  // slab S landed: B_S
+      issue(S + CV_NW - 1);            // into the slot of S-1
+    }
+    vm_barrier<0>();
+  } else if (wave >= 4) {
+    // --------------------------------------------------- activation loaders (4, 5)
+    // 128 rows m0.. shifted by the slab's tap; rows past the tensor read as zero
+    const int aw = wave - 4;
+    const i32x4 ra = buf_rsrc(a.act, (uint32_t)((int64_t)(a.M + 2 * Wp + 2) * a.Ck * 2));
+    uint32_t base[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int r = 8 * (8 * aw + q) + (lane >> 3);
+      const int c = (lane & 7) ^ cv_swz_kc(r);
+      base[q] = (uint32_t)(((int64_t)(m0 + r) * a.Ck + 8 * c) * 2);
+    }
+    const uint32_t d0 = ldsa + (uint32_t)(8 * aw * 1024);
+    auto issue = [&](int S) {
+      const uint32_t slot = d0 + (uint32_t)((S % CV_NA) * CV_ASLOT);
+      uint32_t off = OOB;
+      if (S < nsl) {
+        int c0;
+        const int t = tap_of(S, a.Ck, &c0);
+        const int r = t / 3, s = t - 3 * r;
+        const int shift = TR ? (2 - r) * Wp + 2 - s : r * Wp + s;
+        off = (uint32_t)(((int64_t)shift * a.Ck + c0) * 2);
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) dma16(ra, off == OOB ? OOB : base[q] + off, slot + (uint32_t)(q * 1024));
+    };
+#pragma unroll
+    for (int S = 0; S < CV_NA - 1; ++S) issue(S);
+    for (int S = 0; S < nsl; ++S) {
+      vm_barrier<8 * (CV_NA - 2)>();  // slab S landed: B_S
+      issue(S + CV_NA - 1);           // into the slot of S-1
+    }
+    vm_barrier<0>();
+  } else {
+    // --------------------------------------------------------------- MMA group
+    constexpr int FM = 8;  // 16-position blocks per wave (all 128 positions)
+    const int fi = lane & 15, kg = lane >> 4;
+    const int nb0 = 4 * wave;  // first 16-channel block of the wave
+    uint32_t fa[FM], fx[4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[i] = (uint32_t)((16 * i + fi) * 128);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if constexpr (!TR) {
+        fx[j] = (uint32_t)((16 * (nb0 + j) + fi) * 128);
+      } else {
+        // k-rows 8kg + fi/4 (+4) at channels 16j + 4(fi%4) of quarter `wave`: the transpose
+        // read hands lane fi the four consecutive k of channel 16j + fi
+        const int r = 8 * kg + (fi >> 2);
+        const int c = (2 * j + ((fi >> 1) & 1)) ^ cv_swz_tr(r);
+        fx[j] = (uint32_t)(wave * CV_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
+      }
+    }
+    const int sw = cv_swz_kc(fi);
+
+    f32x4 acc[FM][4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    bf16x8 av[2][FM], wv[2][4];
+    auto read = [&](uint32_t as, uint32_t ws, int s, bf16x8 (&ad)[FM], bf16x8 (&wd)[4]) {
+      const uint32_t co = (uint32_t)(((4 * s + kg) ^ sw) * 16);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        ad[i] = __builtin_bit_cast(bf16x8, *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(as + fa[i] + co));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if constexpr (!TR) {
+          wd[j] = __builtin_bit_cast(bf16x8, *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(ws + fx[j] + co));
+        } else {
+          lds_i16x4 *p = (lds_i16x4 *)(uintptr_t)(ws + fx[j] + (uint32_t)(s * 4096));
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p);
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p + 4 * 128 / 8);
+          wd[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+      }
+    };
+    auto mma = [&](const bf16x8 (&af)[FM], const bf16x8 (&wf)[4]) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], wf[j], acc[i][j], 0, 0, 0);
+    };
+
+    uint32_t as = ldsa, ws = ldsw;  // slots of the slab being read
+    lds_barrier();                  // B_0: slab 0 landed
+    read(as, ws, 0, av[0], wv[0]);
+    for (int S = 0; S < nsl; ++S) {
+      read(as, ws, 1, av[1], wv[1]);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(av[0], wv[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      lds_barrier();  // B_{S+1}: every read of slab S has landed; publish S+1, free S
+      as = ldsa + (uint32_t)(((S + 1) % CV_NA) * CV_ASLOT);
+      ws = ldsw + (uint32_t)(((S + 1) % CV_NW) * CV_WSLOT);
+      read(as, ws, 0, av[0], wv[0]);  // past the last slab this reads a spent slot, unused
+      __builtin_amdgcn_sched_barrier(0);
+      mma(av[1], wv[1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // ---- stage the tile as [position][channel] fp32 (pitch 260 floats: the 64 lanes of
+    // one store hit 64 different banks). All of LDS is free: every wave has passed B_nsl,
+    // and every loader had drained its loads before it.
+    float *stg = reinterpret_cast<float *>(smem);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) stg[(16 * i + 4 * kg + e) * CV_PITCH + 16 * (nb0 + j) + fi] = acc[i][j][e];
+  }
+  lds_barrier();
+  // ---- write the interior positions' rows
+  const float *stg = reinterpret_cast<const float *>(smem);
+  const int Hp = a.H + 2;
+  if (a.out_bf16) {
+    const int ch = tid & 31, sub = tid >> 5;  // 8 channels per thread, 16 rows per pass
+#pragma unroll
+    for (int p = 0; p < CV_BM / 16; ++p) {
+      const int m = 16 * p + sub, P = m0 + m;
+      const int n = P / (Hp * Wp), rem = P - n * Hp * Wp, h = rem / Wp, w = rem - h * Wp;
+      if (P < a.M && h < a.H && w < a.W) {
+        const f32x4 v0 = *reinterpret_cast<const f32x4 *>(stg + m * CV_PITCH + 8 * ch);
+        const f32x4 v1 = *reinterpret_cast<const f32x4 *>(stg + m * CV_PITCH + 8 * ch + 4);
+        u32x4 pk;
+        pk[0] = cvt_pk_bf16(v0[0], v0[1]);
+        pk[1] = cvt_pk_bf16(v0[2], v0[3]);
+        pk[2] = cvt_pk_bf16(v1[0], v1[1]);
+        pk[3] = cvt_pk_bf16(v1[2], v1[3]);
+        uint16_t *o = reinterpret_cast<uint16_t *>(a.out) + ((int64_t)(n * a.H + h) * a.W + w) * CV_BN + 8 * ch;
+        *reinterpret_cast<u32x4 *>(o) = pk;
+      }
+    }
+  } else {
+    const int ch = tid & 63, sub = tid >> 6;  // 4 channels per thread, 8 rows per pass
+#pragma unroll
+    for (int p = 0; p < CV_BM / 8; ++p) {
+      const int m = 8 * p + sub, P = m0 + m;
+      const int n = P / (Hp * Wp), rem = P - n * Hp * Wp, h = rem / Wp, w = rem - h * Wp;
+      if (P < a.M && h < a.H && w < a.W) {
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + m * CV_PITCH + 4 * ch);
+        float *o = reinterpret_cast<float *>(a.out) + ((int64_t)(n * a.H + h) * a.W + w) * CV_BN + 4 * ch;
+        *reinterpret_cast<f32x4 *>(o) = v;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+bool conv_nt_fits(int pass, int N, int H, int W, int Ci, int Co, const void *act, const void *w, const void *out) {
+  const char *env = getenv("IMBD_CONV_NT");  // 0: use the tiled GEMM template instead
+  if (env && atoi(env) == 0) return false;
+  const int Cn = pass == 1 ? Co : Ci, Ck = pass == 1 ? Ci : Co;
+  auto al = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) % 16) == 0; };
+  const int64_t rows = (int64_t)N * (H + 2) * (W + 2) + 2 * (W + 2) + 2 + CV_BM;
+  return (pass == 1 || pass == 2) && N >= 1 && H >= 1 && W >= 1 && Cn == CV_BN && Ck >= 64 && Ck % 64 == 0 &&
+         al(act) && al(w) && al(out) && rows * Ck * 2 < ((int64_t)1 << 31) &&
+         (int64_t)9 * Ci * Co * 2 < ((int64_t)1 << 31);
+}
+
+int run_conv_nt(int pass, int N, int H, int W, int Ci, int Co, const void *act, const void *w, void *out,
+                int out_dtype, hipStream_t s) {
+  CvArgs a;
+  a.act = reinterpret_cast<const uint16_t *>(act);
+  a.w = reinterpret_cast<const uint16_t *>(w);
+  a.out = out;
+  a.out_bf16 = out_dtype == IMBD_BF16 ? 1 : 0;
+  a.H = H;
+  a.W = W;
+  a.Ck = pass == 1 ? Ci : Co;
+  a.Cw = Ci;
+  // positions up to the last interior one of the padded grid
+  a.M = (int)((int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W);
+  a.tiles = (a.M + CV_BM - 1) / CV_BM;
+  const int grid = (a.tiles + 7) / 8 * 8;
+  {
+    LaunchTimer t(pass == 1 ? IMBD_K_CONV_FWD : IMBD_K_CONV_DGRAD, 0, s);
+    if (pass == 1) hipLaunchKernelGGL(conv_nt_kernel<false>, dim3(grid), dim3(512), 0, s, a);
+    else hipLaunchKernelGGL(conv_nt_kernel<true>, dim3(grid), dim3(512), 0, s, a);
+  }
+  return check_launch("conv_nt");
+}
+
+}  // namespace imbd

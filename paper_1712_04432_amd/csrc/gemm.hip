@@ -1048,6 +1048,8 @@ static int conv_launch(int pass, int N, int H, int W, int Ci, int Co, const void
     set_error("conv tile needs C_in and C_out multiples of 64 (got %d, %d)", Ci, Co);
     return IMBD_EUNSUPPORTED;
   }
+  if (pass != 3 && conv_nt_fits(pass, N, H, W, Ci, Co, B, A, out))
+    return run_conv_nt(pass, N, H, W, Ci, Co, B, A, out, out_dtype, s);
   const ConvPlan pl = conv_plan(pass, N, H, W, Ci, Co);
   if ((int64_t)N * (H + 2) * (W + 2) * (Ci > Co ? Ci : Co) >= ((int64_t)1 << 31)) {
     set_error("conv tile too large for 32-bit element offsets");

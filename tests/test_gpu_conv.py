@@ -40,7 +40,12 @@ def _run(imbd, dev, d, out_bf16=False):
 
 
 @pytest.mark.parametrize("N,H,W,Ci,Co", [(2, 5, 7, 64, 128), (1, 9, 4, 128, 64), (2, 6, 6, 128, 128),
-                                         (1, 1, 1, 64, 64), (3, 11, 13, 64, 64)])
+                                         (1, 1, 1, 64, 64), (3, 11, 13, 64, 64),
+                                         # 256 output channels: the large-tile forward / input-gradient
+                                         # kernel (one tile; ragged last tile; idle workgroups of the
+                                         # padded grid; 256 input channels)
+                                         (1, 2, 3, 256, 256), (2, 5, 7, 64, 256), (3, 20, 20, 64, 256),
+                                         (1, 6, 11, 256, 64), (2, 7, 9, 256, 128)])
 @pytest.mark.parametrize("border", [(False, False, False, False), (True, False, True, False),
                                     (True, True, True, True)])
 def test_conv_tile_small(imbd, dev, N, H, W, Ci, Co, border):
