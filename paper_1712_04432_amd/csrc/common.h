@@ -142,6 +142,12 @@ size_t conv_wgrad_ws_bytes(int N, int H, int W, int Ci, int Co);
 bool conv_nt_fits(int pass, int N, int H, int W, int Ci, int Co, const void *act, const void *w, const void *out);
 int run_conv_nt(int pass, int N, int H, int W, int Ci, int Co, const void *act, const void *w, void *out,
                 int out_dtype, hipStream_t s);
+// The weight-gradient pass (256 output channels, C_in a multiple of 128) on the large-tile
+// kernel: fp32 split partials [split][C_out][ldp] into partial, added by the split-K reduce.
+bool conv_wg_fits(int N, int H, int W, int Ci, int Co, const void *x, const void *dy, const void *dw);
+void conv_wg_plan(int N, int H, int W, int Ci, int *splits, int *k_split);
+int run_conv_wg(int N, int H, int W, int Ci, int Co, const void *x, const void *dy_pad, float *partial,
+                int64_t ldp, int64_t sstride, hipStream_t s);
 
 // --------------------------------------------------------------------- host helpers
 void set_error(const char *fmt, ...);

@@ -279,6 +279,221 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
   }
 }
 
+
+// ------------------------------------------------------------------ weight gradient
+// dW[o][tap][c] = sum_P dy[P][o] * x_pad[P + r*(W+2) + s][c] over the positions P of the
+// padded grid whose row and column are inside the tile (Sec. 2.2: the tile's partial of
+// the weight gradient, which the all-reduce over the domain completes). Both operands are
+// position-major, so K = positions and both fragments come from k-row-major LDS slabs
+// through the transpose read. A workgroup owns 256 output channels x 128 input channels
+// of one tap over one range of positions; the ranges are K splits whose fp32 partials the
+// split-K reduce adds in split order. Slabs of 64 positions:
+//  * waves 6-7 load the Delta_Y slab (64 positions x 256 channels, four 64-channel
+//    quarters), rows of positions outside the tile's interior replaced by zeros (their
+//    loads are out of range);
+//  * waves 4-5 load the shifted activation slab (64 positions x 128 channels);
+//  * waves 0-3 each accumulate 128 output channels x 64 input channels.
+struct CwArgs {
+  const uint16_t *x;    // x_pad [N][H+2][W+2][Ci]
+  const uint16_t *dy;   // interior start of dy_pad: dy_pad + ((W+2) + 1) * Co
+  float *partial;       // [split][Co][ldp]: element (tap*Ci + c, o) at o*ldp + tap*Ci + c
+  int64_t ldp, sstride;
+  int H, W, Ci, Co;
+  int M, k_split, splits, tiles;  // positions (up to the last interior one); tiles = 9 * Ci / 128
+};
+
+constexpr int CW_XSLOT = 64 * 256;   // 16 KB: 64 positions x 128 channels
+constexpr int CW_DSLOT = 64 * 512;   // 32 KB: 64 positions x 256 channels
+constexpr int CW_NX = 4, CW_ND = 3;  // ring slots
+constexpr int CW_PITCH = 128 + 4;    // staging row pitch in floats
+
+__global__ void __launch_bounds__(512, 1) conv_wg_kernel(CwArgs a) {
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int DRING = CW_ND * CW_DSLOT, XRING = CW_NX * CW_XSLOT;
+  __shared__ __attribute__((aligned(1024))) char smem[DRING + XRING];
+  static_assert(DRING + XRING <= 160 * 1024, "LDS");
+  static_assert(256 * CW_PITCH * 4 <= DRING + XRING, "staging");
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // padded to a multiple of 8: the tiles of one split (which read the same positions) run
+  // on one XCD
+  const int G = gridDim.x;
+  const int b = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+  if (b >= a.tiles * a.splits) return;
+  const int split = b / a.tiles, tile = b - split * a.tiles;
+  const int tap = tile / (a.Ci / 128), c0 = (tile - tap * (a.Ci / 128)) * 128;
+  const int klo = split * a.k_split, krange = min(a.M, klo + a.k_split) - klo;
+  const int nsl = krange > 0 ? (krange + 63) / 64 : 0;
+  const int Wp = a.W + 2, HWp = (a.H + 2) * Wp;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
+  const uint32_t ldsd = lds0, ldsx = lds0 + DRING;
+
+  if (wave >= 6) {
+    // ---------------------------------------------------- Delta_Y loaders (6, 7)
+    // blocks 16dw..16dw+15 of a slot: quarter h = blk/8, k-rows 8(blk%8)..+7
+    const int dw = wave - 6;
+    const i32x4 rd = buf_rsrc(a.dy, (uint32_t)((int64_t)a.M * a.Co * 2));
+    // the wave's blocks cover quarters 2dw, 2dw+1 of the same 8 row groups g (k-rows
+    // 8g + lane/8); each row's (row, column) in the padded image advances by 64 positions
+    // per slab, kept incrementally (no division per slab)
+    uint32_t col[2][8];
+    int hh[8], ww[8];
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      const int r = 8 * g + (lane >> 3);
+      const int c = (lane & 7) ^ cv_swz_tr(r);
+      col[0][g] = (uint32_t)((64 * (2 * dw) + 8 * c) * 2);
+      col[1][g] = (uint32_t)((64 * (2 * dw + 1) + 8 * c) * 2);
+      const int rem = (klo + r) % HWp;
+      hh[g] = rem / Wp;
+      ww[g] = rem - hh[g] * Wp;
+    }
+    const int adv_h = 64 / Wp, adv_w = 64 - adv_h * Wp, Hp = a.H + 2;
+    auto issue = [&](int S) {
+      const uint32_t slot = ldsd + (uint32_t)((S % CW_ND) * CW_DSLOT);
+#pragma unroll
+      for (int g = 0; g < 8; ++g) {
+        const int r = 8 * g + (lane >> 3), P = klo + S * 64 + r;
+        const bool ok = S < nsl && S * 64 + r < krange && hh[g] < a.H && ww[g] < a.W;
+        const uint32_t off = (uint32_t)P * (uint32_t)(a.Co * 2);
+#pragma unroll
+        for (int hq = 0; hq < 2; ++hq)
+          dma16(rd, ok ? off + col[hq][g] : OOB, slot + (uint32_t)((2 * dw + hq) * CV_QSLOT + g * 1024));
+        // the same row of the next slab: 64 positions on
+        ww[g] += adv_w;
+        hh[g] += adv_h;
+        if (ww[g] >= Wp) {
+          ww[g] -= Wp;
+          ++hh[g];
+        }
+        while (hh[g] >= Hp) hh[g] -= Hp;
+      }
+    };
+#pragma unroll
+    for (int S = 0; S < CW_ND - 1; ++S) issue(S);
+    for (int S = 0; S < nsl; ++S) {
+      vm_barrier<16 * (CW_ND - 2)>();  // slab S landed: B_S
+      issue(S + CW_ND - 1);            // into the slot of S-1
+    }
+    vm_barrier<0>();
+  } else if (wave >= 4) {
+    // --------------------------------------------------- activation loaders (4, 5)
+    // quarter h = blk/8 (channels c0 + 64h ..), k-rows 8(blk%8).. of positions shifted by tap
+    const int xw = wave - 4;
+    const int r3 = tap / 3, s3 = tap - 3 * r3, shift = r3 * Wp + s3;
+    const i32x4 rx = buf_rsrc(a.x, (uint32_t)((int64_t)(a.M + 2 * Wp + 2) * a.Ci * 2));
+    uint32_t base[8], dst[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int blk = 8 * xw + q, g = blk & 7;
+      const int r = 8 * g + (lane >> 3);
+      const int c = (lane & 7) ^ cv_swz_tr(r);
+      base[q] = (uint32_t)(((int64_t)(klo + r + shift) * a.Ci + c0 + 64 * xw + 8 * c) * 2);
+      dst[q] = (uint32_t)(xw * CV_QSLOT + g * 1024);
+    }
+    const uint32_t sstep = (uint32_t)(64 * a.Ci * 2);
+    auto issue = [&](int S) {
+      const uint32_t slot = ldsx + (uint32_t)((S % CW_NX) * CW_XSLOT);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) dma16(rx, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
+    };
+#pragma unroll
+    for (int S = 0; S < CW_NX - 1; ++S) issue(S);
+    for (int S = 0; S < nsl; ++S) {
+      vm_barrier<8 * (CW_NX - 2)>();  // slab S landed: B_S
+      issue(S + CW_NX - 1);           // into the slot of S-1
+    }
+    vm_barrier<0>();
+  } else {
+    // --------------------------------------------------------------- MMA group
+    // wave (wm, wn): output channels 128wm.. (Delta_Y quarters 2wm, 2wm+1), input channels
+    // 64wn.. (activation quarter wn)
+    constexpr int FM = 8;
+    const int fi = lane & 15, kg = lane >> 4;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int r = 8 * kg + (fi >> 2);
+    uint32_t fa[FM], fx[4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int mb = 8 * wm + i, h = mb >> 2, ib = mb & 3;
+      const int c = (2 * ib + ((fi >> 1) & 1)) ^ cv_swz_tr(r);
+      fa[i] = (uint32_t)(h * CV_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = (2 * j + ((fi >> 1) & 1)) ^ cv_swz_tr(r);
+      fx[j] = (uint32_t)(wn * CV_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
+    }
+    f32x4 acc[FM][4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto tr8 = [&](uint32_t addr) {
+      lds_i16x4 *p = (lds_i16x4 *)(uintptr_t)addr;
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p);
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p + 4 * 128 / 8);
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    bf16x8 dv[2][FM], xv[2][4];
+    auto read = [&](uint32_t ds, uint32_t xs, int s, bf16x8 (&dd)[FM], bf16x8 (&xd)[4]) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) dd[i] = tr8(ds + fa[i] + (uint32_t)(s * 4096));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) xd[j] = tr8(xs + fx[j] + (uint32_t)(s * 4096));
+    };
+    auto mma = [&](const bf16x8 (&df)[FM], const bf16x8 (&xf)[4]) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(df[i], xf[j], acc[i][j], 0, 0, 0);
+    };
+    uint32_t ds = ldsd, xs = ldsx;
+    if (nsl > 0) {
+      lds_barrier();  // B_0
+      read(ds, xs, 0, dv[0], xv[0]);
+    }
+    for (int S = 0; S < nsl; ++S) {
+      read(ds, xs, 1, dv[1], xv[1]);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(dv[0], xv[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      lds_barrier();  // B_{S+1}
+      ds = ldsd + (uint32_t)(((S + 1) % CW_ND) * CW_DSLOT);
+      xs = ldsx + (uint32_t)(((S + 1) % CW_NX) * CW_XSLOT);
+      read(ds, xs, 0, dv[0], xv[0]);  // past the last slab this reads a spent slot, unused
+      __builtin_amdgcn_sched_barrier(0);
+      mma(dv[1], xv[1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (nsl == 0) lds_barrier();  // the loaders' B_0 (they pass vm_barrier<0> once)
+    // ---- stage the tile as [output channel][input channel] fp32
+    float *stg = reinterpret_cast<float *>(smem);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          stg[(16 * (8 * wm + i) + 4 * kg + e) * CW_PITCH + 16 * (4 * wn + j) + fi] = acc[i][j][e];
+  }
+  lds_barrier();
+  // ---- partial tile out: 256 rows of 128 floats (512 B), device-scope stores
+  const float *stg = reinterpret_cast<const float *>(smem);
+  float *dst = a.partial + (int64_t)split * a.sstride + tap * a.Ci + c0;
+  const __amdgpu_buffer_rsrc_t prs =
+      __builtin_amdgcn_make_buffer_rsrc(dst, 0, (int)(((int64_t)(a.Co - 1) * a.ldp + 128) * 4), BUF_DW3);
+  const int ch = tid & 31, sub = tid >> 5;
+#pragma unroll
+  for (int p = 0; p < 16; ++p) {
+    const int o = 16 * p + sub;
+    const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + o * CW_PITCH + 4 * ch);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), prs, (uint32_t)((o * a.ldp + 4 * ch) * 4), 0, 16);
+  }
+}
+
 }  // namespace
 
 bool conv_nt_fits(int pass, int N, int H, int W, int Ci, int Co, const void *act, const void *w, const void *out) {
@@ -290,6 +505,49 @@ bool conv_nt_fits(int pass, int N, int H, int W, int Ci, int Co, const void *act
   return (pass == 1 || pass == 2) && N >= 1 && H >= 1 && W >= 1 && Cn == CV_BN && Ck >= 64 && Ck % 64 == 0 &&
          al(act) && al(w) && al(out) && rows * Ck * 2 < ((int64_t)1 << 31) &&
          (int64_t)9 * Ci * Co * 2 < ((int64_t)1 << 31);
+}
+
+bool conv_wg_fits(int N, int H, int W, int Ci, int Co, const void *x, const void *dy, const void *dw) {
+  const char *env = getenv("IMBD_CONV_NT");
+  if (env && atoi(env) == 0) return false;
+  auto al = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) % 16) == 0; };
+  const int64_t rows = (int64_t)N * (H + 2) * (W + 2) + 2 * (W + 2) + 2 + 64;
+  return N >= 1 && H >= 1 && W >= 1 && Co == 256 && Ci >= 128 && Ci % 128 == 0 && al(x) && al(dy) && al(dw) &&
+         rows * (Ci > Co ? Ci : Co) * 2 < ((int64_t)1 << 31);
+}
+
+void conv_wg_plan(int N, int H, int W, int Ci, int *splits, int *k_split) {
+  const int64_t M = (int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W;
+  const int tiles = 9 * Ci / 128;
+  int s = 256 / tiles;
+  if (s < 1) s = 1;
+  int ks = (int)((M + s - 1) / s + 63) / 64 * 64;
+  if (ks < 64) ks = 64;
+  *k_split = ks;
+  *splits = (int)((M + ks - 1) / ks);
+}
+
+int run_conv_wg(int N, int H, int W, int Ci, int Co, const void *x, const void *dy_pad, float *partial,
+                int64_t ldp, int64_t sstride, hipStream_t s) {
+  CwArgs a;
+  a.x = reinterpret_cast<const uint16_t *>(x);
+  a.dy = reinterpret_cast<const uint16_t *>(dy_pad) + (int64_t)(W + 3) * Co;
+  a.partial = partial;
+  a.ldp = ldp;
+  a.sstride = sstride;
+  a.H = H;
+  a.W = W;
+  a.Ci = Ci;
+  a.Co = Co;
+  a.M = (int)((int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W);
+  conv_wg_plan(N, H, W, Ci, &a.splits, &a.k_split);
+  a.tiles = 9 * Ci / 128;
+  const int grid = (a.tiles * a.splits + 7) / 8 * 8;
+  {
+    LaunchTimer t(IMBD_K_CONV_WGRAD, 0, s);
+    hipLaunchKernelGGL(conv_wg_kernel, dim3(grid), dim3(512), 0, s, a);
+  }
+  return check_launch("conv_wg");
 }
 
 int run_conv_nt(int pass, int N, int H, int W, int Ci, int Co, const void *act, const void *w, void *out,

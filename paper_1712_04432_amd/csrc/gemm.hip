@@ -1039,7 +1039,15 @@ ConvPlan conv_plan(int pass, int N, int H, int W, int Ci, int Co) {
 
 size_t conv_wgrad_ws_bytes(int N, int H, int W, int Ci, int Co) {
   if (Ci % 64 || Co % 64) return 0;
-  return conv_plan(3, N, H, W, Ci, Co).ws_bytes;
+  size_t b = conv_plan(3, N, H, W, Ci, Co).ws_bytes;
+  if (N >= 1 && conv_wg_fits(N, H, W, Ci, Co, nullptr, nullptr, nullptr)) {
+    // the large-tile kernel's split partials (it always goes through them)
+    int splits, k_split;
+    conv_wg_plan(N, H, W, Ci, &splits, &k_split);
+    const size_t w = (size_t)splits * (size_t)partial_split_stride(9 * Ci, Co) * sizeof(float);
+    if (w > b) b = w;
+  }
+  return b;
 }
 
 static int conv_launch(int pass, int N, int H, int W, int Ci, int Co, const void *A, const void *B, void *out,
@@ -1050,6 +1058,37 @@ static int conv_launch(int pass, int N, int H, int W, int Ci, int Co, const void
   }
   if (pass != 3 && conv_nt_fits(pass, N, H, W, Ci, Co, B, A, out))
     return run_conv_nt(pass, N, H, W, Ci, Co, B, A, out, out_dtype, s);
+  if (pass == 3 && conv_wg_fits(N, H, W, Ci, Co, A, B, out)) {
+    int splits, k_split;
+    conv_wg_plan(N, H, W, Ci, &splits, &k_split);
+    KArgs g{};
+    g.M = 9 * Ci;
+    g.N = Co;
+    g.splits = splits;
+    g.partial = reinterpret_cast<float *>(ws);
+    g.ldp = partial_ld(g.M);
+    g.sstride = partial_split_stride(g.M, g.N);
+    g.epi = Epilogue{};
+    g.epi.mode = EPI_STORE;
+    g.epi.out = out;
+    g.epi.out_dtype = IMBD_F32;
+    g.epi.ldo = 9 * Ci;
+    const size_t need = (size_t)splits * (size_t)g.sstride * sizeof(float);
+    if (ws == nullptr || ws_bytes < need || (uintptr_t)ws % 16) {
+      set_error("conv weight gradient needs %zu bytes of 16-byte aligned workspace, got %zu", need, ws_bytes);
+      return IMBD_EWORKSPACE;
+    }
+    {
+      const int rc = run_conv_wg(N, H, W, Ci, Co, A, B, g.partial, g.ldp, g.sstride, s);
+      if (rc != IMBD_OK) return rc;
+    }
+    {
+      LaunchTimer t(IMBD_K_SPLITK, 0, s);
+      const dim3 grid((unsigned)((g.M / 8 + 255) / 256), (unsigned)g.N);
+      hipLaunchKernelGGL((splitk_reduce_fast<false, false>), grid, dim3(256), 0, s, g);
+    }
+    return check_launch("conv3x3 reduce");
+  }
   const ConvPlan pl = conv_plan(pass, N, H, W, Ci, Co);
   if ((int64_t)N * (H + 2) * (W + 2) * (Ci > Co ? Ci : Co) >= ((int64_t)1 << 31)) {
     set_error("conv tile too large for 32-bit element offsets");

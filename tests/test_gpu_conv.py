@@ -43,9 +43,13 @@ def _run(imbd, dev, d, out_bf16=False):
                                          (1, 1, 1, 64, 64), (3, 11, 13, 64, 64),
                                          # 256 output channels: the large-tile forward / input-gradient
                                          # kernel (one tile; ragged last tile; idle workgroups of the
-                                         # padded grid; 256 input channels)
+                                         # padded grid; 256 input channels), and for C_in = 256 the
+                                         # weight-gradient kernel
                                          (1, 2, 3, 256, 256), (2, 5, 7, 64, 256), (3, 20, 20, 64, 256),
-                                         (1, 6, 11, 256, 64), (2, 7, 9, 256, 128)])
+                                         (1, 6, 11, 256, 64), (2, 7, 9, 256, 128),
+                                         # C_in a multiple of 128 as well: the split-K weight-gradient
+                                         # kernel (one split of 8 positions; 22 splits)
+                                         (2, 5, 7, 128, 256), (3, 20, 20, 128, 256)])
 @pytest.mark.parametrize("border", [(False, False, False, False), (True, False, True, False),
                                     (True, True, True, True)])
 def test_conv_tile_small(imbd, dev, N, H, W, Ci, Co, border):
