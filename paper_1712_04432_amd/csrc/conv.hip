@@ -32,12 +32,12 @@
 namespace imbd {
 namespace {
 
-constexpr int CV_BM = 128;             // positions per workgroup
+constexpr int CV_BM = 128;             // positions per workgroup, at most (16 FM, FM = 7 or 8)
 constexpr int CV_BN = 256;             // channels of the output per workgroup
 constexpr int CV_KS = 64;              // k per slab: 64 channels of one tap
 constexpr int CV_NA = 4;               // activation ring slots
 constexpr int CV_NW = 3;               // weight ring slots
-constexpr int CV_ASLOT = CV_BM * 128;  // 16 KB
+constexpr int CV_ASLOT = CV_BM * 128;  // 16 KB (the slot of the largest tile)
 constexpr int CV_WSLOT = CV_BN * 128;  // 32 KB
 constexpr int CV_QSLOT = 64 * 128;     // one 64-channel quarter of a transposed weight slab
 constexpr int CV_PITCH = CV_BN + 4;    // staging row pitch in floats (1040 B)
@@ -54,9 +54,11 @@ struct CvArgs {
 __device__ __forceinline__ int cv_swz_kc(int r) { return r & 7; }
 __device__ __forceinline__ int cv_swz_tr(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
 
-// TR: input gradient (W read transposed); else forward.
-template <bool TR>
+// TR: input gradient (W read transposed); else forward. FM: 16-position blocks per tile
+// (7 or 8; the host picks the one that fills the last round of workgroups best).
+template <bool TR, int FM>
 __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
+  constexpr int BM = 16 * FM;
   constexpr uint32_t OOB = 0x80000000u;
   constexpr int WRING = CV_NW * CV_WSLOT, ARING = CV_NA * CV_ASLOT;
   __shared__ __attribute__((aligned(1024))) char smem[WRING + ARING];
@@ -70,7 +72,7 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
   const int G = gridDim.x;
   const int b = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
   if (b >= a.tiles) return;
-  const int m0 = b * CV_BM;
+  const int m0 = b * BM;
   const int Wp = a.W + 2;
   const int nsl = 9 * a.Ck / CV_KS;
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
@@ -131,17 +133,18 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
     vm_barrier<0>();
   } else if (wave >= 4) {
     // --------------------------------------------------- activation loaders (4, 5)
-    // 128 rows m0.. shifted by the slab's tap; rows past the tensor read as zero
+    // BM rows m0.. shifted by the slab's tap; rows past the tensor read as zero. Wave aw
+    // fills the 1 KB blocks FM*aw .. FM*aw + FM-1 (8 rows each).
     const int aw = wave - 4;
     const i32x4 ra = buf_rsrc(a.act, (uint32_t)((int64_t)(a.M + 2 * Wp + 2) * a.Ck * 2));
-    uint32_t base[8];
+    uint32_t base[FM];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int r = 8 * (8 * aw + q) + (lane >> 3);
+    for (int q = 0; q < FM; ++q) {
+      const int r = 8 * (FM * aw + q) + (lane >> 3);
       const int c = (lane & 7) ^ cv_swz_kc(r);
       base[q] = (uint32_t)(((int64_t)(m0 + r) * a.Ck + 8 * c) * 2);
     }
-    const uint32_t d0 = ldsa + (uint32_t)(8 * aw * 1024);
+    const uint32_t d0 = ldsa + (uint32_t)(FM * aw * 1024);
     auto issue = [&](int S) {
       const uint32_t slot = d0 + (uint32_t)((S % CV_NA) * CV_ASLOT);
       uint32_t off = OOB;
@@ -153,18 +156,17 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
         off = (uint32_t)(((int64_t)shift * a.Ck + c0) * 2);
       }
 #pragma unroll
-      for (int q = 0; q < 8; ++q) dma16(ra, off == OOB ? OOB : base[q] + off, slot + (uint32_t)(q * 1024));
+      for (int q = 0; q < FM; ++q) dma16(ra, off == OOB ? OOB : base[q] + off, slot + (uint32_t)(q * 1024));
     };
 #pragma unroll
     for (int S = 0; S < CV_NA - 1; ++S) issue(S);
     for (int S = 0; S < nsl; ++S) {
-      vm_barrier<8 * (CV_NA - 2)>();  // slab S landed: B_S
+      vm_barrier<FM * (CV_NA - 2)>();  // slab S landed: B_S
       issue(S + CV_NA - 1);           // into the slot of S-1
     }
     vm_barrier<0>();
   } else {
     // --------------------------------------------------------------- MMA group
-    constexpr int FM = 8;  // 16-position blocks per wave (all 128 positions)
     const int fi = lane & 15, kg = lane >> 4;
     const int nb0 = 4 * wave;  // first 16-channel block of the wave
     uint32_t fa[FM], fx[4];
@@ -249,7 +251,7 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
   if (a.out_bf16) {
     const int ch = tid & 31, sub = tid >> 5;  // 8 channels per thread, 16 rows per pass
 #pragma unroll
-    for (int p = 0; p < CV_BM / 16; ++p) {
+    for (int p = 0; p < FM; ++p) {
       const int m = 16 * p + sub, P = m0 + m;
       const int n = P / (Hp * Wp), rem = P - n * Hp * Wp, h = rem / Wp, w = rem - h * Wp;
       if (P < a.M && h < a.H && w < a.W) {
@@ -267,7 +269,7 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
   } else {
     const int ch = tid & 63, sub = tid >> 6;  // 4 channels per thread, 8 rows per pass
 #pragma unroll
-    for (int p = 0; p < CV_BM / 8; ++p) {
+    for (int p = 0; p < 2 * FM; ++p) {
       const int m = 8 * p + sub, P = m0 + m;
       const int n = P / (Hp * Wp), rem = P - n * Hp * Wp, h = rem / Wp, w = rem - h * Wp;
       if (P < a.M && h < a.H && w < a.W) {
@@ -563,12 +565,21 @@ int run_conv_nt(int pass, int N, int H, int W, int Ci, int Co, const void *act, 
   a.Cw = Ci;
   // positions up to the last interior one of the padded grid
   a.M = (int)((int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W);
-  a.tiles = (a.M + CV_BM - 1) / CV_BM;
+  // tile of 112 or 128 positions: the one with less work in the rounds of 256 workgroups
+  // (32 x 56 x 56: 961 tiles of 112 in 4 rounds against 841 of 128, also in 4 rounds)
+  auto rounds_work = [&](int fm) { return (int64_t)((a.M + 16 * fm - 1) / (16 * fm) + 255) / 256 * fm; };
+  const int fm = rounds_work(7) < rounds_work(8) ? 7 : 8;
+  a.tiles = (a.M + 16 * fm - 1) / (16 * fm);
   const int grid = (a.tiles + 7) / 8 * 8;
   {
     LaunchTimer t(pass == 1 ? IMBD_K_CONV_FWD : IMBD_K_CONV_DGRAD, 0, s);
-    if (pass == 1) hipLaunchKernelGGL(conv_nt_kernel<false>, dim3(grid), dim3(512), 0, s, a);
-    else hipLaunchKernelGGL(conv_nt_kernel<true>, dim3(grid), dim3(512), 0, s, a);
+    if (pass == 1) {
+      if (fm == 7) hipLaunchKernelGGL((conv_nt_kernel<false, 7>), dim3(grid), dim3(512), 0, s, a);
+      else hipLaunchKernelGGL((conv_nt_kernel<false, 8>), dim3(grid), dim3(512), 0, s, a);
+    } else {
+      if (fm == 7) hipLaunchKernelGGL((conv_nt_kernel<true, 7>), dim3(grid), dim3(512), 0, s, a);
+      else hipLaunchKernelGGL((conv_nt_kernel<true, 8>), dim3(grid), dim3(512), 0, s, a);
+    }
   }
   return check_launch("conv_nt");
 }

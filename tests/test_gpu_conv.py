@@ -88,6 +88,26 @@ def test_conv_tile_full_size_sampled(imbd, dev, border):
     assert torch.isfinite(y).all().item() and torch.isfinite(dx).all().item() and torch.isfinite(dw).all().item()
 
 
+def test_conv_tile_128_position_tiles_sampled(imbd, dev):
+    """A tile size for which the forward kernel takes 128-position tiles (240 tiles fill
+    one round of workgroups; 112-position tiles would need two): sampled outputs of the
+    three passes."""
+    _flush("conv 8x60x60 128->256")
+    N, H, W, Ci, Co = 8, 60, 60, 128, 256
+    d = make_conv_inputs(N, H, W, Ci, Co, seed=9, border=(True, False, False, True))
+    xv, wv, dyv = bf16_values(d["x_bits"]), bf16_values(d["w_bits"]), bf16_values(d["dy_bits"])
+    y, dx, dw = _run(imbd, dev, d)
+    rng = np.random.default_rng(3)
+    yi = np.concatenate([rng.choice(y.numel(), 300, replace=False), [0, y.numel() - 1]])
+    assert nrm_err(host(y).reshape(-1)[yi], oracle.conv3x3_fwd_at(xv, wv, yi)) < 1e-5
+    xi = rng.choice(dx.numel(), 200, replace=False)
+    assert nrm_err(host(dx).reshape(-1)[xi], oracle.conv3x3_dgrad_at(dyv, wv, xi)) < 1e-5
+    wi = rng.choice(dw.numel(), 24, replace=False)
+    assert nrm_err(host(dw).reshape(-1)[wi], oracle.conv3x3_wgrad_at(xv, dyv, wi)) < 1e-5
+    import torch
+    assert torch.isfinite(y).all().item() and torch.isfinite(dx).all().item() and torch.isfinite(dw).all().item()
+
+
 def test_conv_stitched_domain_split(imbd, dev):
     """Domain parallelism on one GPU: a 2x2 split of a zero-padded image with exchanged
     halos (cut from the full padded tensor) reproduces the full-image conv, the summed
