@@ -40,6 +40,8 @@ constexpr int CPOL_MASTER_LD = 2;
 constexpr int CPOL_MASTER_ST = 2 | 16;
 constexpr int CPOL_COPY_ST = 16;
 
+constexpr int KMAX_SAMPLES = 256;  // samples of the Delta_Y block resident at a time
+
 struct DwArgs {
   const uint16_t *X;   // [K][ldx]  rows are samples, M = d_in columns
   const uint16_t *DY;  // [K][lddy] N = d_out columns
@@ -84,6 +86,12 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
   const int full = a.tiles_m / gpb, rem = a.tiles_m % gpb;
   const int nmy = b < tiles ? full + ((grp + full) % gpb < rem ? 1 : 0) : 0;
   const int TK = (a.K + BK - 1) / BK;
+  // Batches past 256 samples: the Delta_Y block holds one chunk of 256 samples (8 slabs)
+  // at a time and is reloaded whenever the next slab starts another chunk (the first of
+  // every tile included), 2 barriers per reload.
+  const int nch = (TK + 7) / 8;
+  const bool multi = nch > 1;
+  auto reloads = [&](int it) { return multi ? nch - (it == nmy - 1 ? 1 : 0) : 0; };
   const int n0 = (b % a.tiles_n) * BN;
   auto tile_m0 = [&](int it) { return (gpb * it + (grp + it) % gpb) * BM; };
 
@@ -103,16 +111,18 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
     // read touches then cover every bank exactly twice. A wave's 1 KB load covers 4 rows:
     // lane i fills row 4q + i/16, stored chunk i%16, from source chunk (i%16) ^ swz(row).
     const int dr = lane >> 4, dc = lane & 15;
-    // resident Delta_Y block: wave w loads rows 64w..64w+63, 16 loads of 4 rows
-    {
+    // resident Delta_Y block (samples 256 ch .. 256 ch + 255): wave w loads rows
+    // 64w..64w+63, 16 loads of 4 rows
+    auto load_dy = [&](int ch) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int r = 64 * wave + 4 * q + dr;
         const int scol = 8 * (dc ^ (2 * dr + 8 * ((q >> 1) & 1)));  // source column of the lane's chunk
-        const uint32_t off = n0 + scol < a.N ? (uint32_t)((r * a.lddy + n0 + scol) * 2) : OOB;
+        const uint32_t off = n0 + scol < a.N ? (uint32_t)(((KMAX * ch + r) * a.lddy + n0 + scol) * 2) : OOB;
         dma16(rdy, off, __builtin_amdgcn_readfirstlane(ldy + (uint32_t)((64 * wave + 4 * q) * ROWB)));
       }
-    }
+    };
+    load_dy(0);
     // X slabs: wave w fills rows 8w..8w+7 of each slab (two 4-row loads)
     const int dcol = 8 * (dc ^ (2 * dr + 8 * (wave & 1)));
     const uint32_t xstep = (uint32_t)(BK * a.ldx * 2), xh = (uint32_t)(4 * a.ldx * 2);
@@ -253,7 +263,7 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
       bias_pending = false;
     };
 
-    int c_ks = 0;
+    int c_ks = 0, c_it = 0;
     uint32_t c_slot = 0, c_krow = 0;
     i16x4 fa[FM][2], fb[FN][2], ga[FM][2], gb[FN][2];
     read_slab(c_slot, c_krow, fa, fb);
@@ -265,17 +275,22 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
       issue();
       c_slot = c_slot + XSLAB == NS * XSLAB ? 0u : c_slot + XSLAB;
       const bool tile_end = ++c_ks == TK;
-      c_krow += BK * ROWB;
-      if (tile_end) {
-        c_ks = 0;
-        c_krow = 0;
-      }
+      if (tile_end) c_ks = 0;
+      c_krow = (uint32_t)((c_ks & 7) * BK * ROWB);
       // The MFMAs of slab s go first: the transpose reads of slab s+1 then run while
       // the matrix pipe works, with no wait between them.
       mma(ca, cb);
       __builtin_amdgcn_sched_barrier(0);
+      if (multi && (c_ks & 7) == 0 && !(tile_end && c_it == nmy - 1)) {
+        lds_barrier();        // every wave is done reading the current chunk
+        load_dy(c_ks >> 3);   // the next slab's chunk
+        vm_barrier<0>();      // landed in every wave
+      }
       read_slab(c_slot, c_krow, na, nb);
-      if (tile_end) handoff();
+      if (tile_end) {
+        ++c_it;
+        handoff();
+      }
     };
     // Two steps per trip so that the fragment sets alternate without copies.
     for (int s = 0; s < total; s += 2) {
@@ -359,6 +374,7 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
       }
       if (have) {
         for (int ch = CHUNKS; ch < TK; ++ch) lds_barrier();
+        for (int q = 0; q < 2 * reloads(it); ++q) lds_barrier();  // the MMA group's Delta_Y reloads
         lds_barrier();  // staging free
         lds_barrier();  // staging full
       }
@@ -373,7 +389,7 @@ bool dw_sgd_fits(const GemmProblem &p) {
   const Epilogue &e = p.epi;
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   return p.dtype == IMBD_BF16 && !p.a_kc && !p.b_kc && e.mode == EPI_SGD && e.out2 && !e.mask && !e.bias &&
-         !e.relu && p.K > 0 && p.K <= 256 && p.M > 0 && p.N > 0 && p.N <= 256 * 128 && p.M % 8 == 0 &&
+         !e.relu && p.K > 0 && p.K <= 2048 && p.M > 0 && p.N > 0 && p.N <= 256 * 128 && p.M % 8 == 0 &&
          p.N % 8 == 0 && al(p.A, 16) && al(p.B, 16) && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
          al(e.out, 16) && e.ldo % 4 == 0 && al(e.out2, 8) && e.ldo2 % 4 == 0 && e.ldo < (1 << 21) &&
          e.ldo2 < (1 << 21) && (int64_t)p.K * p.lda * 2 < ((int64_t)1 << 31) &&
@@ -395,7 +411,10 @@ int run_dw_sgd(const GemmProblem &p, hipStream_t s) {
   d.ldw16 = p.epi.ldo2;
   d.lr = p.epi.lr;
   d.alpha = p.epi.alpha;
-  d.db_mode = p.db_mode;
+  // past 256 samples the Delta_Y block is never whole in LDS: the bias gradient gets the
+  // column-sum kernel instead
+  const bool bias_apart = p.K > KMAX_SAMPLES && p.db_mode != 0;
+  d.db_mode = bias_apart ? 0 : p.db_mode;
   d.db_out = p.db_out;
   d.bias = p.bias;
   d.db_alpha = p.db_alpha;
@@ -410,7 +429,10 @@ int run_dw_sgd(const GemmProblem &p, hipStream_t s) {
     LaunchTimer t(p.kclass, p.layer, s, true);
     hipExtLaunchKernelGGL(dw_sgd_kernel, dim3(grid), dim3(512), 0, s, t.start(), t.stop(), 0, d);
   }
-  return check_launch("dw_sgd");
+  const int rc = check_launch("dw_sgd");
+  if (rc != IMBD_OK || !bias_apart) return rc;
+  return run_bias_grad(IMBD_BF16, p.N, p.K, p.B, p.ldb, p.db_alpha, p.db_mode == 1 ? p.db_out : nullptr,
+                       p.db_mode == 2 ? p.bias : nullptr, p.bias_lr, s, p.layer);
 }
 
 }  // namespace imbd

@@ -119,6 +119,47 @@ __global__ void __launch_bounds__(256)
   }
 }
 
+// The same column sums for bf16 Delta_Y with 16-byte rows chunks (8 columns): 64 columns per
+// workgroup, thread t sums chunk t%8 over the rows r = t/8 + 32i in ascending order (eight
+// loads in flight per batch), then the 32 row phases are added in phase order.
+__global__ void __launch_bounds__(256)
+    bias_grad_wide(int M, int B, const uint16_t *__restrict__ dy, int64_t lddy, float alpha,
+                   float *__restrict__ db_out, float *__restrict__ bias, float lr) {
+  __shared__ float part[32][64 + 4];
+  const int j = threadIdx.x & 7, q = threadIdx.x >> 3;
+  const int m0 = blockIdx.x * 64 + 8 * j;
+  const bool live = m0 < M;  // M % 8 == 0: a chunk is wholly in or out
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int r0 = q; r0 < B; r0 += 32 * 8) {
+    u32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int r = r0 + 32 * u;
+      v[u] = live && r < B ? *reinterpret_cast<const u32x4 *>(dy + (int64_t)r * lddy + m0) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[2 * e] += bf16_to_f32((uint16_t)(v[u][e] & 0xffffu));
+        s[2 * e + 1] += bf16_to_f32((uint16_t)(v[u][e] >> 16));
+      }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) part[q][8 * j + e] = s[e];
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int m = blockIdx.x * 64 + threadIdx.x;
+    float t = 0.f;
+    for (int k = 0; k < 32; ++k) t += part[k][threadIdx.x];
+    if (m < M) {
+      const float g = alpha * t;
+      if (db_out) db_out[m] = g;
+      if (bias) bias[m] = fmaf(-lr, g, bias[m]);
+    }
+  }
+}
+
 // w <- w - step * g (one fp32 rounding), optional bf16 copy. Four elements per thread.
 __global__ void __launch_bounds__(256)
     sgd_kernel(float *__restrict__ w, uint16_t *__restrict__ w16, const float *__restrict__ g,
@@ -207,7 +248,10 @@ int run_bias_grad(int dtype, int M, int B, const void *dy, int64_t lddy, float a
                   float *db_out, float *bias_sgd, float lr, hipStream_t s, int layer) {
   if (M <= 0) return IMBD_OK;
   LaunchTimer t(IMBD_K_BIAS, layer, s);
-  if (dtype == IMBD_BF16)
+  if (dtype == IMBD_BF16 && M % 8 == 0 && lddy % 8 == 0 && (uintptr_t)dy % 16 == 0)
+    hipLaunchKernelGGL(bias_grad_wide, dim3((M + 63) / 64), dim3(256), 0, s, M, B,
+                       reinterpret_cast<const uint16_t *>(dy), lddy, alpha, db_out, bias_sgd, lr);
+  else if (dtype == IMBD_BF16)
     hipLaunchKernelGGL(bias_grad_kernel<uint16_t>, dim3((M + 63) / 64), dim3(256), 0, s, M, B,
                        reinterpret_cast<const uint16_t *>(dy), lddy, alpha, db_out, bias_sgd, lr);
   else

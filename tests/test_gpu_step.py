@@ -99,7 +99,9 @@ def test_bf16_one_step_matches_mirrored_oracle(imbd, dev, dims, B):
 
 
 @pytest.mark.parametrize("dims,B", [((2056, 2104, 24), 72), ((136, 8, 16), 8), ((4096, 1000, 128), 256),
-                                    ((136, 8, 16), 1), ((264, 128, 24), 5)])
+                                    ((136, 8, 16), 1), ((264, 128, 24), 5),
+                                    # past 256 samples the Delta_Y block is reloaded per 256-sample chunk
+                                    ((264, 128, 24), 300), ((1032, 264, 16), 777)])
 def test_bf16_fused_update_matches_oracle(imbd, dev, dims, B):
     """The fused weight update (Eq. (1) applied inside the weight-gradient product) on
     shapes that give the persistent update kernel several tiles per workgroup (17 x 17
