@@ -114,7 +114,7 @@ bool skinny_softmax_fits(const GemmProblem &p);
 int run_skinny_softmax(const GemmProblem &p, void *ws, const int32_t *labels, float inv_batch, float *row_loss,
                        void *dz, int64_t lddz, int dz_dtype, hipStream_t s);
 int run_loss_mean(int B, const float *row_loss, float inv_batch, float *loss, hipStream_t s);
-// The persistent fused weight-gradient + update kernel (bf16, K <= 256): whether it
+// The persistent fused weight-gradient + update kernel (bf16, K <= 2048): whether it
 // takes the problem, and the launch.
 bool dw_sgd_fits(const GemmProblem &p);
 int run_dw_sgd(const GemmProblem &p, hipStream_t s);

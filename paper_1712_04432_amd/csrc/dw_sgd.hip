@@ -6,7 +6,7 @@
 // the bias gradient (column sums of Delta_Y) applied the same way.
 //
 // The update streams 10 bytes per weight through HBM (fp32 master read and written, bf16
-// copy written) while the product itself is small (K <= 256), so the kernel is built
+// copy written) while the product itself is small (K = batch), so the kernel is built
 // around that stream. Persistent workgroups, one per CU, of eight waves in two groups:
 //  * waves 0-3 (MMA group) keep the workgroup's Delta_Y column block resident in LDS
 //    (the grid is a multiple of the column-block count, so all tiles of a workgroup
