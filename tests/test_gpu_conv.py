@@ -152,6 +152,17 @@ def test_conv_stitched_domain_split(imbd, dev):
     assert nrm_err(dw, dw_full) < 1e-5
 
 
+def test_conv_tile_is_deterministic(imbd, dev):
+    """The three passes of the 256-channel kernels twice on the same inputs: identical bits
+    (the weight gradient's split partials are added in split order)."""
+    d = make_conv_inputs(2, 9, 10, 128, 256, seed=4)
+    a = _run(imbd, dev, d)
+    b = _run(imbd, dev, d)
+    import torch
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
 def test_conv_errors(imbd, dev):
     import torch
     x = torch.zeros((1, 4, 4, 48), dtype=torch.bfloat16, device=dev)
