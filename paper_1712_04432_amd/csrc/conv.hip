@@ -16,12 +16,12 @@
 // (csrc/skinny.hip): both operands travel through LDS in 64-k slabs written by buffer
 // loads that go straight to LDS in whole 128-byte lines, loader waves with their own
 // memory counters, one barrier per slab, XOR-swizzled 16-byte chunks:
-//  * waves 4-5 stream the activation slab (128 shifted rows x 128 B) through a 4-slot ring;
-//  * waves 6-7 stream the weight slab (256 channels x 64 k) through a 3-slot ring: rows of
-//    W for the forward pass, k-rows of W (64 output channels of one tap x 256 input
+//  * waves 8-9 stream the activation slab (128 shifted rows x 128 B) through a 4-slot ring;
+//  * waves 10-11 stream the weight slab (256 channels x 64 k) through a 3-slot ring: rows
+//    of W for the forward pass, k-rows of W (64 output channels of one tap x 256 input
 //    channels, as four 64-channel quarters) for the input gradient, whose fragments then
 //    come from the gfx950 LDS transpose read;
-//  * waves 0-3 each accumulate 128 positions x 64 channels in registers.
+//  * waves 0-7, two per SIMD, each accumulate 64 positions x 64 channels in registers.
 // After the last slab the tile goes through LDS ([position][channel], fp32) and is written
 // as whole 512-byte (bf16) or 1 KB (fp32) rows of the interior positions.
 
@@ -32,12 +32,12 @@
 namespace imbd {
 namespace {
 
-constexpr int CV_BM = 128;             // positions per workgroup, at most (16 FM, FM = 7 or 8)
+constexpr int CV_BM = 128;             // positions per workgroup
 constexpr int CV_BN = 256;             // channels of the output per workgroup
 constexpr int CV_KS = 64;              // k per slab: 64 channels of one tap
 constexpr int CV_NA = 4;               // activation ring slots
 constexpr int CV_NW = 3;               // weight ring slots
-constexpr int CV_ASLOT = CV_BM * 128;  // 16 KB (the slot of the largest tile)
+constexpr int CV_ASLOT = CV_BM * 128;  // 16 KB
 constexpr int CV_WSLOT = CV_BN * 128;  // 32 KB
 constexpr int CV_QSLOT = 64 * 128;     // one 64-channel quarter of a transposed weight slab
 constexpr int CV_PITCH = CV_BN + 4;    // staging row pitch in floats (1040 B)
@@ -54,11 +54,16 @@ struct CvArgs {
 __device__ __forceinline__ int cv_swz_kc(int r) { return r & 7; }
 __device__ __forceinline__ int cv_swz_tr(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
 
-// TR: input gradient (W read transposed); else forward. FM: 16-position blocks per tile
-// (7 or 8; the host picks the one that fills the last round of workgroups best).
-template <bool TR, int FM>
-__global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
-  constexpr int BM = 16 * FM;
+// TR: input gradient (W read transposed); else forward. Eight MMA waves, two per SIMD, so
+// that one computes while the other waits for its fragments or the slab barrier (with one
+// per SIMD the matrix pipe was busy ~40% of the time): wave w takes the positions of half
+// w%2 and the channels of quarter w/2. The loader waves follow the MMA waves.
+template <bool TR>
+__global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
+  constexpr int NMW = 8;
+  constexpr int FM = 8, BM = 16 * FM;  // 128 positions
+  constexpr int NT = 64 * (NMW + 4);
+  constexpr int FMW = FM / 2;          // position blocks per MMA wave
   constexpr uint32_t OOB = 0x80000000u;
   constexpr int WRING = CV_NW * CV_WSLOT, ARING = CV_NA * CV_ASLOT;
   __shared__ __attribute__((aligned(1024))) char smem[WRING + ARING];
@@ -85,9 +90,9 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
     return t;
   };
 
-  if (wave >= 6) {
-    // ------------------------------------------------------- weight loaders (6, 7)
-    const int ww = wave - 6;
+  if (wave >= NMW + 2) {
+    // --------------------------------------------------------------- weight loaders
+    const int ww = wave - NMW - 2;
     const i32x4 rw = buf_rsrc(a.w, (uint32_t)((int64_t)9 * a.Ck * CV_BN * 2));
     uint32_t base[16];
     uint32_t dst[16];
@@ -131,11 +136,11 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
       issue(S + CV_NW - 1);            // into the slot of S-1
     }
     vm_barrier<0>();
-  } else if (wave >= 4) {
-    // --------------------------------------------------- activation loaders (4, 5)
+  } else if (wave >= NMW) {
+    // ----------------------------------------------------------- activation loaders
     // BM rows m0.. shifted by the slab's tap; rows past the tensor read as zero. Wave aw
     // fills the 1 KB blocks FM*aw .. FM*aw + FM-1 (8 rows each).
-    const int aw = wave - 4;
+    const int aw = wave - NMW;
     const i32x4 ra = buf_rsrc(a.act, (uint32_t)((int64_t)(a.M + 2 * Wp + 2) * a.Ck * 2));
     uint32_t base[FM];
 #pragma unroll
@@ -168,35 +173,37 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
   } else {
     // --------------------------------------------------------------- MMA group
     const int fi = lane & 15, kg = lane >> 4;
-    const int nb0 = 4 * wave;  // first 16-channel block of the wave
-    uint32_t fa[FM], fx[4];
+    const int nq = wave >> 1;          // channel quarter of the wave
+    const int mb0 = FMW * (wave & 1);  // first position block
+    const int nb0 = 4 * nq;                                // first 16-channel block
+    uint32_t fa[FMW], fx[4];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) fa[i] = (uint32_t)((16 * i + fi) * 128);
+    for (int i = 0; i < FMW; ++i) fa[i] = (uint32_t)((16 * (mb0 + i) + fi) * 128);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       if constexpr (!TR) {
         fx[j] = (uint32_t)((16 * (nb0 + j) + fi) * 128);
       } else {
-        // k-rows 8kg + fi/4 (+4) at channels 16j + 4(fi%4) of quarter `wave`: the transpose
+        // k-rows 8kg + fi/4 (+4) at channels 16j + 4(fi%4) of quarter nq: the transpose
         // read hands lane fi the four consecutive k of channel 16j + fi
         const int r = 8 * kg + (fi >> 2);
         const int c = (2 * j + ((fi >> 1) & 1)) ^ cv_swz_tr(r);
-        fx[j] = (uint32_t)(wave * CV_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
+        fx[j] = (uint32_t)(nq * CV_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
       }
     }
     const int sw = cv_swz_kc(fi);
 
-    f32x4 acc[FM][4];
+    f32x4 acc[FMW][4];
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FMW; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    bf16x8 av[2][FM], wv[2][4];
-    auto read = [&](uint32_t as, uint32_t ws, int s, bf16x8 (&ad)[FM], bf16x8 (&wd)[4]) {
+    bf16x8 av[2][FMW], wv[2][4];
+    auto read = [&](uint32_t as, uint32_t ws, int s, bf16x8 (&ad)[FMW], bf16x8 (&wd)[4]) {
       const uint32_t co = (uint32_t)(((4 * s + kg) ^ sw) * 16);
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < FMW; ++i)
         ad[i] = __builtin_bit_cast(bf16x8, *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(as + fa[i] + co));
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -210,9 +217,9 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
         }
       }
     };
-    auto mma = [&](const bf16x8 (&af)[FM], const bf16x8 (&wf)[4]) {
+    auto mma = [&](const bf16x8 (&af)[FMW], const bf16x8 (&wf)[4]) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < FMW; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], wf[j], acc[i][j], 0, 0, 0);
     };
@@ -238,21 +245,20 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
     // and every loader had drained its loads before it.
     float *stg = reinterpret_cast<float *>(smem);
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FMW; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) stg[(16 * i + 4 * kg + e) * CV_PITCH + 16 * (nb0 + j) + fi] = acc[i][j][e];
+        for (int e = 0; e < 4; ++e) stg[(16 * (mb0 + i) + 4 * kg + e) * CV_PITCH + 16 * (nb0 + j) + fi] = acc[i][j][e];
   }
   lds_barrier();
   // ---- write the interior positions' rows
   const float *stg = reinterpret_cast<const float *>(smem);
   const int Hp = a.H + 2;
   if (a.out_bf16) {
-    const int ch = tid & 31, sub = tid >> 5;  // 8 channels per thread, 16 rows per pass
-#pragma unroll
-    for (int p = 0; p < FM; ++p) {
-      const int m = 16 * p + sub, P = m0 + m;
+    const int ch = tid & 31, sub = tid >> 5;  // 8 channels per thread, NT/32 rows per pass
+    for (int m = sub; m < BM; m += NT / 32) {
+      const int P = m0 + m;
       const int n = P / (Hp * Wp), rem = P - n * Hp * Wp, h = rem / Wp, w = rem - h * Wp;
       if (P < a.M && h < a.H && w < a.W) {
         const f32x4 v0 = *reinterpret_cast<const f32x4 *>(stg + m * CV_PITCH + 8 * ch);
@@ -267,10 +273,9 @@ __global__ void __launch_bounds__(512, 1) conv_nt_kernel(CvArgs a) {
       }
     }
   } else {
-    const int ch = tid & 63, sub = tid >> 6;  // 4 channels per thread, 8 rows per pass
-#pragma unroll
-    for (int p = 0; p < 2 * FM; ++p) {
-      const int m = 8 * p + sub, P = m0 + m;
+    const int ch = tid & 63, sub = tid >> 6;  // 4 channels per thread, NT/64 rows per pass
+    for (int m = sub; m < BM; m += NT / 64) {
+      const int P = m0 + m;
       const int n = P / (Hp * Wp), rem = P - n * Hp * Wp, h = rem / Wp, w = rem - h * Wp;
       if (P < a.M && h < a.H && w < a.W) {
         const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + m * CV_PITCH + 4 * ch);
@@ -565,21 +570,12 @@ int run_conv_nt(int pass, int N, int H, int W, int Ci, int Co, const void *act, 
   a.Cw = Ci;
   // positions up to the last interior one of the padded grid
   a.M = (int)((int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W);
-  // tile of 112 or 128 positions: the one with less work in the rounds of 256 workgroups
-  // (32 x 56 x 56: 961 tiles of 112 in 4 rounds against 841 of 128, also in 4 rounds)
-  auto rounds_work = [&](int fm) { return (int64_t)((a.M + 16 * fm - 1) / (16 * fm) + 255) / 256 * fm; };
-  const int fm = rounds_work(7) < rounds_work(8) ? 7 : 8;
-  a.tiles = (a.M + 16 * fm - 1) / (16 * fm);
+  a.tiles = (a.M + CV_BM - 1) / CV_BM;
   const int grid = (a.tiles + 7) / 8 * 8;
   {
     LaunchTimer t(pass == 1 ? IMBD_K_CONV_FWD : IMBD_K_CONV_DGRAD, 0, s);
-    if (pass == 1) {
-      if (fm == 7) hipLaunchKernelGGL((conv_nt_kernel<false, 7>), dim3(grid), dim3(512), 0, s, a);
-      else hipLaunchKernelGGL((conv_nt_kernel<false, 8>), dim3(grid), dim3(512), 0, s, a);
-    } else {
-      if (fm == 7) hipLaunchKernelGGL((conv_nt_kernel<true, 7>), dim3(grid), dim3(512), 0, s, a);
-      else hipLaunchKernelGGL((conv_nt_kernel<true, 8>), dim3(grid), dim3(512), 0, s, a);
-    }
+    if (pass == 1) hipLaunchKernelGGL(conv_nt_kernel<false>, dim3(grid), dim3(768), 0, s, a);
+    else hipLaunchKernelGGL(conv_nt_kernel<true>, dim3(grid), dim3(768), 0, s, a);
   }
   return check_launch("conv_nt");
 }
