@@ -49,9 +49,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
+def measured_traffic(workload: str):
     """HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE/WRITE_SIZE
-    runs, kept only while the kernel source is the one the counters were taken on."""
+    runs, kept only for the workload they were taken on and while the kernel source is the
+    one the counters were taken on."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     kv = {}
@@ -59,7 +60,7 @@ def measured_traffic():
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("kernel_source_hash") != kernel_source_hash():
+    if kv.get("kernel_source_hash") != kernel_source_hash() or kv.get("workload") != workload:
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
@@ -465,7 +466,7 @@ def main():
     tflops = flops / (ms_step * 1e-3) / 1e12
     dom_bytes = dw_sgd_bytes(cfg.dims[1], cfg.dims[0], cfg.batch)
     achieved = dom_bytes / (k_avg_ms * 1e-3) / 1e9
-    traffic = measured_traffic()
+    traffic = measured_traffic(cfg.name)
     result = {
         "metric": METRIC,
         "value": round(tflops, 3),
@@ -488,7 +489,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4),
                      "traffic": traffic,
-                     "kernel": "layer-1 weight gradient with fused SGD (4096x9216 update, K=256)",
+                     "kernel": f"layer-1 weight gradient with fused SGD ({cfg.dims[1]}x{cfg.dims[0]} update, "
+                               f"K={cfg.batch})",
                      "algorithmic_bytes_per_launch": dom_bytes, "avg_launch_ms": round(k_avg_ms, 5),
                      "launches_timed": n_launch},
         "loss_first": round(loss0, 6),
