@@ -282,7 +282,7 @@ static int fwd_impl(const imbd_mlp_desc *d, const imbd_layer *layers, const void
       e.out_dtype = IMBD_F32;
     }
     e.ldo = d->dims[i];
-    if (i == L && gemm_plan(p).cfg < 0 && skinny_softmax_fits(p)) {
+    if (i == L && gemm_plan(p).cfg == PLAN_SKINNY && skinny_softmax_fits(p)) {
       // top layer: split reduce, bias and softmax cross-entropy in one pass
       if (lay.partial_bytes < gemm_plan(p).ws_bytes) FAIL(IMBD_EWORKSPACE, "partial-sum region too small");
       float *rl = reinterpret_cast<float *>(at(ws, lay.rowloss));

@@ -87,8 +87,10 @@ struct GemmProblem {
 };
 
 // Launch plan chosen for a product (a pure function of the shapes).
+constexpr int PLAN_SKINNY = -1;  // GemmPlan::cfg of the skinny-batch kernel
+constexpr int PLAN_WIDE = -2;    // ... of the wide-batch forward / Delta_X kernel
 struct GemmPlan {
-  int cfg;       // tile configuration index
+  int cfg;       // tile configuration index, or PLAN_SKINNY / PLAN_WIDE
   int bm, bn;    // tile sizes
   int splits;    // K splits (1 = no partial sums)
   int k_split;   // K elements per split (multiple of the K tile)
@@ -107,6 +109,12 @@ bool skinny_fits(const GemmProblem &p);
 void skinny_plan(const GemmProblem &p, int *splits, int *k_split);
 int run_skinny(const GemmProblem &p, void *ws, hipStream_t s);
 size_t skinny_ws_bytes(const GemmProblem &p);
+// Forward / Delta_X products for batches above 256 (bf16, B operand stored [n][k]):
+// whether the large-tile kernel takes the problem, its K split (slabs of 64 per split),
+// and the launch (partials into partial when splits > 1; the caller adds them).
+bool wide_fits(const GemmProblem &p);
+void wide_plan(const GemmProblem &p, int *splits, int *kps);
+int run_wide(const GemmProblem &p, float *partial, int64_t ldp, int64_t sstride, hipStream_t s);
 // The top layer's forward product with its split reduce fused into softmax cross-entropy
 // (logits stored to p.epi.out, per-sample losses and the logits' gradient); the loss mean
 // is left to the caller.

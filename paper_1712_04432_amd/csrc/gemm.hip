@@ -845,10 +845,20 @@ GemmPlan gemm_plan(const GemmProblem &p) {
   if (skinny_fits(p) && env_int("IMBD_SKINNY_OFF", 0) == 0) {
     // the skinny-batch product always goes through fp32 partials (one per K split)
     skinny_plan(p, &pl.splits, &pl.k_split);
-    pl.cfg = -1;
+    pl.cfg = PLAN_SKINNY;
     pl.bm = 64;
     pl.bn = 256;
     pl.ws_bytes = skinny_ws_bytes(p);
+    return pl;
+  }
+  if (wide_fits(p)) {
+    int kps;
+    wide_plan(p, &pl.splits, &kps);
+    pl.cfg = PLAN_WIDE;
+    pl.bm = 256;
+    pl.bn = 128;
+    pl.k_split = 64 * kps;
+    pl.ws_bytes = pl.splits > 1 ? (size_t)pl.splits * (size_t)partial_split_stride(p.M, p.N) * sizeof(float) : 0;
     return pl;
   }
   const int esz = p.dtype == IMBD_BF16 ? 2 : 4;
@@ -919,7 +929,7 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     return IMBD_EINVAL;
   }
   const GemmPlan pl = gemm_plan(p);
-  if (p.aux_loss && (pl.cfg >= 0 || p.M <= 0 || p.N <= 0)) {
+  if (p.aux_loss && (pl.cfg != PLAN_SKINNY || p.M <= 0 || p.N <= 0)) {
     // only the skinny reduce carries the side job; elsewhere it gets its own launch
     GemmProblem q = p;
     q.aux_loss = nullptr;
@@ -937,7 +947,7 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     set_error("workspace must be 16-byte aligned");
     return IMBD_EINVAL;
   }
-  if (pl.cfg < 0) return run_skinny(p, ws, s);
+  if (pl.cfg == PLAN_SKINNY) return run_skinny(p, ws, s);
   const int esz = p.dtype == IMBD_BF16 ? 2 : 4;
   KArgs g;
   g.A = p.A;
@@ -978,6 +988,11 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   g.ldp = partial_ld(p.M);
   g.sstride = partial_split_stride(p.M, p.N);
 
+  if (pl.cfg == PLAN_WIDE) {
+    int rc = run_wide(p, g.partial, g.ldp, g.sstride, s);
+    if (rc == IMBD_OK && pl.splits > 1) rc = launch_reduce(p, g, s);
+    return rc;
+  }
   // The fused update of a bf16 weight gradient runs on its own persistent kernel.
   if (dw_sgd_fits(p) && env_int("IMBD_DW_GENERIC", 0) == 0) return run_dw_sgd(p, s);
   const TileCfg &c = kCfgs[pl.cfg];

@@ -112,6 +112,9 @@ LOCAL_SHAPES = [
     (256, 784, 64), (128, 256, 64), (10, 128, 64),             # the 784-256-128-10 layers
     (1024, 4096, 64), (250, 4096, 64),                          # 4 x 16 grid blocks
     (130, 200, 70), (37, 100, 13), (1, 1, 1), (64, 64, 64), (129, 65, 257), (3, 8, 5),
+    # past 256 samples, bf16: the wide-batch product kernel, ragged in every dimension
+    # (forward split over K; Delta_X whole), and a forward split 8 ways
+    (264, 1032, 777), (512, 4096, 300),
     (200, 1000, 128),
 ]
 
@@ -194,6 +197,34 @@ def test_local_fwd_strided_views(imbd, dev):
     ref = oracle.affine_fwd(Wv[100:200, 8:520], Xv[48:72, 8:520])
     assert nrm_err(host(yblk), ref) < 1e-5
     assert torch.count_nonzero(ybig[:, :100]).item() == 0 and torch.count_nonzero(ybig[:, 200:]).item() == 0
+
+
+def test_local_wide_batch_strided_views(imbd, dev):
+    """The wide-batch products on blocks passed as views (leading dimensions above the
+    row lengths, output a column block of a larger array)."""
+    import torch
+    rng = np.random.default_rng(4)
+    Wf = rng.standard_normal((300, 520)).astype(np.float32)
+    Xf = rng.standard_normal((300, 520)).astype(np.float32)
+    DYf = rng.standard_normal((300, 264)).astype(np.float32)
+    Wb, Xb, DYb = to_bf16_bits(Wf), to_bf16_bits(Xf), to_bf16_bits(DYf)
+    wd, xd, dyd = dev_bf16_bits(Wb, dev), dev_bf16_bits(Xb, dev), dev_bf16_bits(DYb, dev)
+    Wv, Xv, DYv = bf16_values(Wb), bf16_values(Xb), bf16_values(DYb)
+    wblk, xblk = wd[100:300, 8:520], xd[:, 8:520]
+    ybig = torch.zeros((300, 400), device=dev)
+    yblk = ybig[:, 100:300]
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(0, 1, 200, 512, 300), 16), dtype=torch.uint8, device=dev)
+    imbd.mlp_local_fwd(wblk, xblk, yblk, 1, 1, ws=ws)
+    ref = oracle.affine_fwd(Wv[100:300, 8:520], Xv[:, 8:520])
+    assert nrm_err(host(yblk), ref) < 1e-5
+    assert torch.count_nonzero(ybig[:, :100]).item() == 0 and torch.count_nonzero(ybig[:, 300:]).item() == 0
+    # Delta_X of a 264 x 512 block (view of rows 8..272 of a 300 x 520 array): W^T Delta_Y
+    w2 = wd[8:272, 8:520]
+    dx = torch.empty((300, 512), device=dev)
+    dw = torch.empty((264, 512), device=dev)
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(1, 1, 264, 512, 300), 16), dtype=torch.uint8, device=dev)
+    imbd.mlp_local_bwd(w2, dyd, xblk, dw, 1, 1, dx_part=dx, mask_relu=False, ws=ws)
+    assert nrm_err(host(dx), oracle.input_grad(Wv[8:272, 8:520], DYv)) < 1e-5
 
 
 def test_local_bwd_empty_block_writes_zero_partials(imbd, dev):

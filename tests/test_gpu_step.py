@@ -78,7 +78,10 @@ def test_fp32_mlp784_fused_update(imbd, dev):
 
 
 @pytest.mark.parametrize("dims,B", [((576, 320, 256, 100), 64), ((33, 17, 5), 3), ((8, 1, 2), 1),
-                                    ((1000, 300, 200, 10), 96), ((4096, 1000, 128), 32)])
+                                    ((1000, 300, 200, 10), 96), ((4096, 1000, 128), 32),
+                                    # past 256 samples (the wide-batch products): ragged
+                                    # batch, rows and K, split and whole, fp32 logits
+                                    ((1032, 264, 136), 777), ((1032, 520, 264, 136), 300)])
 def test_bf16_one_step_matches_mirrored_oracle(imbd, dev, dims, B):
     import torch
     cfg = scaled_mlp(dims, B, "bf16")
