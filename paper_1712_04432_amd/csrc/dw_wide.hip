@@ -1,0 +1,290 @@
+// Fused weight gradient + SGD update of a fully connected layer for batches above 256
+// samples (bf16 operands, fp32 masters):
+//   Delta_W[o][i] = sum_b Delta_Y[b][o] X[b][i]      (Sec. 1, K = the batch)
+//   w[o][i] -= lr * alpha * Delta_W[o][i];  w16[o][i] = bf16(w[o][i])   (Eq. (1))
+// The bias gradient (column sums of Delta_Y) is left to the column-sum kernel.
+//
+// At these batch sizes the product (2 x batch flops per weight) outweighs the update's
+// 10 bytes per weight, so the kernel takes the large-tile layout of the conv tile's
+// weight-gradient kernel (csrc/conv.hip), with the update done by the epilogue of each
+// tile (K is never split: the update needs the whole sum). A workgroup owns 256 output
+// rows o x 128 input columns i; both operands are sample-major, so K = samples and both
+// fragments come from k-row slabs through the gfx950 LDS transpose read. Slabs of 64
+// samples:
+//  * waves 6-7 load the Delta_Y slab (64 samples x 256 columns, four 64-column quarters)
+//    through a 3-slot ring;
+//  * waves 4-5 load the X slab (64 samples x 128 columns, two quarters) through a 4-slot
+//    ring;
+//  * waves 0-3 each accumulate 128 rows o x 64 columns i in registers.
+// Samples past the batch are past the end of the buffer descriptors and read as zero;
+// columns past M or N only reach outputs that are not stored.
+// Then the tile goes through LDS ([o][i], fp32) and all eight waves update it: non-
+// temporal master loads, non-temporal device-scope master stores and device-scope stores
+// of the bf16 copy, as in the small-batch update kernel (csrc/dw_sgd.hip), which keeps
+// the masters out of the caches and the new copy in the MALL for the next forward.
+
+#include <stdlib.h>
+
+#include "cdna4.h"
+
+namespace imbd {
+namespace {
+
+constexpr int DL_XSLOT = 64 * 256;   // 16 KB: 64 samples x 128 columns
+constexpr int DL_DSLOT = 64 * 512;   // 32 KB: 64 samples x 256 columns
+constexpr int DL_QSLOT = 64 * 128;   // one 64-column quarter of a slab
+constexpr int DL_NX = 4, DL_ND = 3;  // ring slots
+constexpr int DL_PITCH = 128 + 4;    // staging row pitch in floats
+constexpr int DL_GM = 8;             // o tiles per launch-order group
+constexpr int CPOL_MASTER_LD = 2;      // nt
+constexpr int CPOL_MASTER_ST = 2 | 16;  // nt, device scope
+constexpr int CPOL_COPY_ST = 16;        // device scope
+
+struct DlArgs {
+  const uint16_t *X;   // [K][ldx], M columns
+  const uint16_t *DY;  // [K][lddy], N columns
+  int64_t ldx, lddy;
+  uint32_t x_bytes, dy_bytes;
+  int M, N, K;
+  float *w;            // [N][ldw] fp32 masters
+  uint16_t *w16;       // [N][ldw16] bf16 copy
+  int64_t ldw, ldw16;
+  uint32_t w_bytes, w16_bytes;
+  float lr, alpha;
+  int tiles_o, tiles_i;
+};
+
+__device__ __forceinline__ int dl_swz(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
+
+__global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int DRING = DL_ND * DL_DSLOT, XRING = DL_NX * DL_XSLOT;
+  __shared__ __attribute__((aligned(1024))) char smem[DRING + XRING];
+  static_assert(DRING + XRING <= 160 * 1024, "LDS");
+  static_assert(256 * DL_PITCH * 4 <= DRING + XRING, "staging");
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // grid padded to a multiple of 8; each XCD takes a contiguous range of the launch order,
+  // in which tiles come in groups of DL_GM o tiles x all i tiles (shared slabs in L2)
+  const int G = gridDim.x;
+  int L = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+  if (L >= a.tiles_o * a.tiles_i) return;
+  const int og = L / (DL_GM * a.tiles_i);
+  const int gsz = min(DL_GM, a.tiles_o - og * DL_GM);
+  L -= og * DL_GM * a.tiles_i;
+  const int it = L / gsz, ot = og * DL_GM + (L - it * gsz);
+  const int o0 = ot * 256, i0 = it * 128;
+  const int nsl = (a.K + 63) / 64;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
+  const uint32_t ldsd = lds0, ldsx = lds0 + DRING;
+
+  if (wave >= 6) {
+    // ---------------------------------------------------- Delta_Y loaders (6, 7)
+    // the wave's blocks: quarters 2dw, 2dw+1, k-rows 8g + lane/8 of the slab
+    const int dw = wave - 6;
+    const i32x4 rd = buf_rsrc(a.DY, a.dy_bytes);
+    uint32_t base[16], dst[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int h = 2 * dw + (q >> 3), g = q & 7;
+      const int r = 8 * g + (lane >> 3);
+      const int c = (lane & 7) ^ dl_swz(r);
+      base[q] = (uint32_t)(((int64_t)r * a.lddy + o0 + 64 * h + 8 * c) * 2);
+      dst[q] = (uint32_t)(h * DL_QSLOT + g * 1024);
+    }
+    const uint32_t sstep = (uint32_t)(64 * a.lddy * 2);
+    auto issue = [&](int S) {
+      const uint32_t slot = ldsd + (uint32_t)((S % DL_ND) * DL_DSLOT);
+#pragma unroll
+      for (int q = 0; q < 16; ++q) dma16(rd, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
+    };
+#pragma unroll
+    for (int S = 0; S < DL_ND - 1; ++S) issue(S);
+    for (int S = 0; S < nsl; ++S) {
+      vm_barrier<16 * (DL_ND - 2)>();  // slab S landed: B_S
+      issue(S + DL_ND - 1);            // into the slot of S-1
+    }
+    vm_barrier<0>();
+  } else if (wave >= 4) {
+    // --------------------------------------------------------- X loaders (4, 5)
+    const int xw = wave - 4;
+    const i32x4 rx = buf_rsrc(a.X, a.x_bytes);
+    uint32_t base[8], dst[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int r = 8 * q + (lane >> 3);
+      const int c = (lane & 7) ^ dl_swz(r);
+      base[q] = (uint32_t)(((int64_t)r * a.ldx + i0 + 64 * xw + 8 * c) * 2);
+      dst[q] = (uint32_t)(xw * DL_QSLOT + q * 1024);
+    }
+    const uint32_t sstep = (uint32_t)(64 * a.ldx * 2);
+    auto issue = [&](int S) {
+      const uint32_t slot = ldsx + (uint32_t)((S % DL_NX) * DL_XSLOT);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) dma16(rx, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
+    };
+#pragma unroll
+    for (int S = 0; S < DL_NX - 1; ++S) issue(S);
+    for (int S = 0; S < nsl; ++S) {
+      vm_barrier<8 * (DL_NX - 2)>();  // slab S landed: B_S
+      issue(S + DL_NX - 1);           // into the slot of S-1
+    }
+    vm_barrier<0>();
+  } else {
+    // --------------------------------------------------------------- MMA group
+    // wave (wm, wn): rows o 128wm.. (Delta_Y quarters 2wm, 2wm+1), columns i 64wn..
+    constexpr int FM = 8;
+    const int fi = lane & 15, kg = lane >> 4;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int r = 8 * kg + (fi >> 2);
+    uint32_t fa[FM], fx[4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int mb = 8 * wm + i, h = mb >> 2, ib = mb & 3;
+      const int c = (2 * ib + ((fi >> 1) & 1)) ^ dl_swz(r);
+      fa[i] = (uint32_t)(h * DL_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = (2 * j + ((fi >> 1) & 1)) ^ dl_swz(r);
+      fx[j] = (uint32_t)(wn * DL_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
+    }
+    f32x4 acc[FM][4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto tr8 = [&](uint32_t addr) {
+      lds_i16x4 *p = (lds_i16x4 *)(uintptr_t)addr;
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p);
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p + 4 * 128 / 8);
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    bf16x8 dv[2][FM], xv[2][4];
+    auto read = [&](uint32_t ds, uint32_t xs, int s, bf16x8 (&dd)[FM], bf16x8 (&xd)[4]) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) dd[i] = tr8(ds + fa[i] + (uint32_t)(s * 4096));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) xd[j] = tr8(xs + fx[j] + (uint32_t)(s * 4096));
+    };
+    auto mma = [&](const bf16x8 (&df)[FM], const bf16x8 (&xf)[4]) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(df[i], xf[j], acc[i][j], 0, 0, 0);
+    };
+    uint32_t ds = ldsd, xs = ldsx;
+    lds_barrier();  // B_0
+    read(ds, xs, 0, dv[0], xv[0]);
+    for (int S = 0; S < nsl; ++S) {
+      read(ds, xs, 1, dv[1], xv[1]);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(dv[0], xv[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      lds_barrier();  // B_{S+1}
+      ds = ldsd + (uint32_t)(((S + 1) % DL_ND) * DL_DSLOT);
+      xs = ldsx + (uint32_t)(((S + 1) % DL_NX) * DL_XSLOT);
+      read(ds, xs, 0, dv[0], xv[0]);  // past the last slab this reads a spent slot, unused
+      __builtin_amdgcn_sched_barrier(0);
+      mma(dv[1], xv[1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // ---- stage the tile as [o][i] fp32
+    float *stg = reinterpret_cast<float *>(smem);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          stg[(16 * (8 * wm + i) + 4 * kg + e) * DL_PITCH + 16 * (4 * wn + j) + fi] = acc[i][j][e];
+  }
+  lds_barrier();
+  // ---- the update: row o0 + 16p + sub, columns i0 + 4ch .. +3, eight rows' masters in
+  // flight per thread
+  const float *stg = reinterpret_cast<const float *>(smem);
+  const int ch = tid & 31, sub = tid >> 5;
+  const int i = i0 + 4 * ch;
+  if (i >= a.M) return;
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(a.w, 0, (int)a.w_bytes, BUF_DW3);
+  const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(a.w16, 0, (int)a.w16_bytes, BUF_DW3);
+  const float step = a.lr;
+#pragma unroll
+  for (int p0 = 0; p0 < 16; p0 += 8) {
+    f32x4 wold[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int o = o0 + 16 * (p0 + u) + sub;
+      // rows past N: an offset past the descriptor (reads zero, the store is dropped)
+      const uint32_t off = o < a.N ? (uint32_t)(((int64_t)o * a.ldw + i) * 4) : OOB;
+      wold[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, off, 0, CPOL_MASTER_LD));
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int ol = 16 * (p0 + u) + sub, o = o0 + ol;
+      const f32x4 g = *reinterpret_cast<const f32x4 *>(stg + ol * DL_PITCH + 4 * ch);
+      f32x4 nw;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) nw[e] = fmaf(-step, a.alpha * g[e], wold[u][e]);
+      u32x2 pk;
+      pk[0] = cvt_pk_bf16(nw[0], nw[1]);
+      pk[1] = cvt_pk_bf16(nw[2], nw[3]);
+      const uint32_t offw = o < a.N ? (uint32_t)(((int64_t)o * a.ldw + i) * 4) : OOB;
+      const uint32_t offh = o < a.N ? (uint32_t)(((int64_t)o * a.ldw16 + i) * 2) : OOB;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, nw), rw, offw, 0, CPOL_MASTER_ST);
+      __builtin_amdgcn_raw_buffer_store_b64(pk, rh, offh, 0, CPOL_COPY_ST);
+    }
+  }
+}
+
+}  // namespace
+
+bool dw_wide_fits(const GemmProblem &p) {
+  const char *env = getenv("IMBD_DW_WIDE_MIN_K");  // smallest batch that takes this kernel
+  const int min_k = (env && *env) ? atoi(env) : 257;
+  const Epilogue &e = p.epi;
+  auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
+  const int64_t lim = (int64_t)1 << 31;  // bytes in one buffer descriptor
+  return p.dtype == IMBD_BF16 && !p.a_kc && !p.b_kc && e.mode == EPI_SGD && e.out2 && !e.mask && !e.bias &&
+         !e.relu && p.K >= min_k && p.K > 0 && p.M > 0 && p.N > 0 && p.M % 8 == 0 && al(p.A, 16) &&
+         al(p.B, 16) && p.lda % 8 == 0 && p.ldb % 8 == 0 && p.lda >= p.M && p.ldb >= p.N && al(e.out, 16) &&
+         e.ldo % 4 == 0 && e.ldo >= p.M && al(e.out2, 8) && e.ldo2 % 4 == 0 && e.ldo2 >= p.M &&
+         ((int64_t)(p.K - 1) * p.lda + p.M) * 2 < lim && ((int64_t)(p.K - 1) * p.ldb + p.N) * 2 < lim &&
+         ((int64_t)(p.N - 1) * e.ldo + p.M) * 4 < lim && ((int64_t)(p.N - 1) * e.ldo2 + p.M) * 2 < lim;
+}
+
+int run_dw_wide(const GemmProblem &p, hipStream_t s) {
+  DlArgs a;
+  a.X = reinterpret_cast<const uint16_t *>(p.A);
+  a.DY = reinterpret_cast<const uint16_t *>(p.B);
+  a.ldx = p.lda;
+  a.lddy = p.ldb;
+  a.x_bytes = (uint32_t)(((int64_t)(p.K - 1) * p.lda + p.M) * 2);
+  a.dy_bytes = (uint32_t)(((int64_t)(p.K - 1) * p.ldb + p.N) * 2);
+  a.M = p.M;
+  a.N = p.N;
+  a.K = p.K;
+  a.w = reinterpret_cast<float *>(p.epi.out);
+  a.w16 = p.epi.out2;
+  a.ldw = p.epi.ldo;
+  a.ldw16 = p.epi.ldo2;
+  a.w_bytes = (uint32_t)(((int64_t)(p.N - 1) * p.epi.ldo + p.M) * 4);
+  a.w16_bytes = (uint32_t)(((int64_t)(p.N - 1) * p.epi.ldo2 + p.M) * 2);
+  a.lr = p.epi.lr;
+  a.alpha = p.epi.alpha;
+  a.tiles_o = (p.N + 255) / 256;
+  a.tiles_i = (p.M + 127) / 128;
+  const int grid = (a.tiles_o * a.tiles_i + 7) / 8 * 8;
+  {
+    LaunchTimer t(p.kclass, p.layer, s);
+    hipLaunchKernelGGL(dw_wide_kernel, dim3(grid), dim3(512), 0, s, a);
+  }
+  int rc = check_launch("dw_wide");
+  if (rc != IMBD_OK || p.db_mode == 0) return rc;
+  return run_bias_grad(IMBD_BF16, p.N, p.K, p.B, p.ldb, p.db_alpha, p.db_mode == 1 ? p.db_out : nullptr,
+                       p.db_mode == 2 ? p.bias : nullptr, p.bias_lr, s, p.layer);
+}
+
+}  // namespace imbd
