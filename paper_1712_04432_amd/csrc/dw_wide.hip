@@ -2,7 +2,8 @@
 // samples (bf16 operands, fp32 masters):
 //   Delta_W[o][i] = sum_b Delta_Y[b][o] X[b][i]      (Sec. 1, K = the batch)
 //   w[o][i] -= lr * alpha * Delta_W[o][i];  w16[o][i] = bf16(w[o][i])   (Eq. (1))
-// The bias gradient (column sums of Delta_Y) is left to the column-sum kernel.
+// (or, for the unfused and local backward passes, alpha * Delta_W stored as fp32). The
+// bias gradient (column sums of Delta_Y) is left to the column-sum kernel.
 //
 // At these batch sizes the product (2 x batch flops per weight) outweighs the update's
 // 10 bytes per weight, so the kernel takes the large-tile layout of the conv tile's
@@ -56,6 +57,8 @@ struct DlArgs {
 
 __device__ __forceinline__ int dl_swz(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
 
+// SGD: update the masters and the bf16 copy; else store alpha * Delta_W to w (fp32).
+template <bool SGD>
 __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
   constexpr uint32_t OOB = 0x80000000u;
   constexpr int DRING = DL_ND * DL_DSLOT, XRING = DL_NX * DL_XSLOT;
@@ -214,16 +217,23 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
     const int o = o0 + 16 * u + sub;
     return (colok && o < a.N) ? (uint32_t)(((int64_t)o * a.ldw + i) * 4) : OOB;
   };
-  f32x4 wold[16];
-  auto load_masters = [&]() {
-#pragma unroll
-    for (int u = 0; u < 16; ++u)
-      wold[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, offw(u), 0, CPOL_MASTER_LD));
-  };
-  lds_barrier();
-  load_masters();
-  if (!colok) return;
   const float *stg = reinterpret_cast<const float *>(smem);
+  if constexpr (!SGD) {
+    lds_barrier();
+    if (!colok) return;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const f32x4 g = *reinterpret_cast<const f32x4 *>(stg + (16 * u + sub) * DL_PITCH + 4 * ch);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a.alpha * g), rw, offw(u), 0, 0);
+    }
+    return;
+  }
+  f32x4 wold[16];
+  lds_barrier();
+#pragma unroll
+  for (int u = 0; u < 16; ++u)
+    wold[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, offw(u), 0, CPOL_MASTER_LD));
+  if (!colok) return;
 #pragma unroll
   for (int u = 0; u < 16; ++u) {
     const int ol = 16 * u + sub, o = o0 + ol;
@@ -248,12 +258,16 @@ bool dw_wide_fits(const GemmProblem &p) {
   const Epilogue &e = p.epi;
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const int64_t lim = (int64_t)1 << 31;  // bytes in one buffer descriptor
-  return p.dtype == IMBD_BF16 && !p.a_kc && !p.b_kc && e.mode == EPI_SGD && e.out2 && !e.mask && !e.bias &&
-         !e.relu && p.K >= min_k && p.K > 0 && p.M > 0 && p.N > 0 && p.M % 8 == 0 && al(p.A, 16) &&
-         al(p.B, 16) && p.lda % 8 == 0 && p.ldb % 8 == 0 && p.lda >= p.M && p.ldb >= p.N && al(e.out, 16) &&
-         e.ldo % 4 == 0 && e.ldo >= p.M && al(e.out2, 8) && e.ldo2 % 4 == 0 && e.ldo2 >= p.M &&
-         ((int64_t)(p.K - 1) * p.lda + p.M) * 2 < lim && ((int64_t)(p.K - 1) * p.ldb + p.N) * 2 < lim &&
-         ((int64_t)(p.N - 1) * e.ldo + p.M) * 4 < lim && ((int64_t)(p.N - 1) * e.ldo2 + p.M) * 2 < lim;
+  if (p.dtype != IMBD_BF16 || p.a_kc || p.b_kc || e.mask || e.bias || e.relu || p.K < min_k || p.K <= 0 ||
+      p.M <= 0 || p.N <= 0 || p.M % 8 || !al(p.A, 16) || !al(p.B, 16) || p.lda % 8 || p.ldb % 8 ||
+      p.lda < p.M || p.ldb < p.N || !al(e.out, 16) || e.ldo % 4 || e.ldo < p.M)
+    return false;
+  if (((int64_t)(p.K - 1) * p.lda + p.M) * 2 >= lim || ((int64_t)(p.K - 1) * p.ldb + p.N) * 2 >= lim ||
+      ((int64_t)(p.N - 1) * e.ldo + p.M) * 4 >= lim)
+    return false;
+  if (e.mode == EPI_STORE) return e.out_dtype == IMBD_F32;  // alpha * Delta_W, fp32
+  return e.mode == EPI_SGD && e.out2 && al(e.out2, 8) && e.ldo2 % 4 == 0 && e.ldo2 >= p.M &&
+         ((int64_t)(p.N - 1) * e.ldo2 + p.M) * 2 < lim;
 }
 
 int run_dw_wide(const GemmProblem &p, hipStream_t s) {
@@ -272,7 +286,8 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   a.ldw = p.epi.ldo;
   a.ldw16 = p.epi.ldo2;
   a.w_bytes = (uint32_t)(((int64_t)(p.N - 1) * p.epi.ldo + p.M) * 4);
-  a.w16_bytes = (uint32_t)(((int64_t)(p.N - 1) * p.epi.ldo2 + p.M) * 2);
+  const bool sgd = p.epi.mode == EPI_SGD;
+  a.w16_bytes = sgd ? (uint32_t)(((int64_t)(p.N - 1) * p.epi.ldo2 + p.M) * 2) : 0;
   a.lr = p.epi.lr;
   a.alpha = p.epi.alpha;
   a.tiles_o = (p.N + 255) / 256;
@@ -280,7 +295,8 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   const int grid = (a.tiles_o * a.tiles_i + 7) / 8 * 8;
   {
     LaunchTimer t(p.kclass, p.layer, s);
-    hipLaunchKernelGGL(dw_wide_kernel, dim3(grid), dim3(512), 0, s, a);
+    if (sgd) hipLaunchKernelGGL(dw_wide_kernel<true>, dim3(grid), dim3(512), 0, s, a);
+    else hipLaunchKernelGGL(dw_wide_kernel<false>, dim3(grid), dim3(512), 0, s, a);
   }
   int rc = check_launch("dw_wide");
   if (rc != IMBD_OK || p.db_mode == 0) return rc;

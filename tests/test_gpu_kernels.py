@@ -225,6 +225,9 @@ def test_local_wide_batch_strided_views(imbd, dev):
     ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(1, 1, 264, 512, 300), 16), dtype=torch.uint8, device=dev)
     imbd.mlp_local_bwd(w2, dyd, xblk, dw, 1, 1, dx_part=dx, mask_relu=False, ws=ws)
     assert nrm_err(host(dx), oracle.input_grad(Wv[8:272, 8:520], DYv)) < 1e-5
+    # the weight-gradient partial of the same call (fp32 store, scale 1/b)
+    rdw, _ = oracle.weight_grad(DYv, Xv[:, 8:520], 1.0 / 300)
+    assert nrm_err(host(dw), rdw) < 1e-5
 
 
 def test_local_bwd_empty_block_writes_zero_partials(imbd, dev):
