@@ -310,18 +310,52 @@ __global__ void __launch_bounds__(256) skinny_reduce(SkReduceArgs g) {
   const float v[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
   const int cnt = VEC ? 8 : min(8, g.M - m);
   float x[8];
+  if constexpr (VEC) {
+    // bias, mask and output rows are whole and aligned (checked on the host)
+    float bb[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (e.bias) {
+      const f32x4 b0 = *reinterpret_cast<const f32x4 *>(e.bias + m);
+      const f32x4 b1 = *reinterpret_cast<const f32x4 *>(e.bias + m + 4);
+      bb[0] = b0[0]; bb[1] = b0[1]; bb[2] = b0[2]; bb[3] = b0[3];
+      bb[4] = b1[0]; bb[5] = b1[1]; bb[6] = b1[2]; bb[7] = b1[3];
+    }
+    bool keep[8] = {true, true, true, true, true, true, true, true};
+    if (e.mask) {
+      const int64_t off = (int64_t)n * e.ldmask + m;
+      if (e.mask_dtype == IMBD_BF16) {
+        const u32x4 mk = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint16_t *>(e.mask) + off);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    if (i < cnt) {
-      float y = e.alpha * v[i] + (e.bias ? e.bias[m + i] : 0.0f);
-      if (e.relu) y = y > 0.0f ? y : 0.0f;
-      if (e.mask) {
-        const int64_t off = (int64_t)n * e.ldmask + m + i;
-        const float mk = e.mask_dtype == IMBD_BF16 ? bf16_to_f32(reinterpret_cast<const uint16_t *>(e.mask)[off])
-                                                   : reinterpret_cast<const float *>(e.mask)[off];
-        if (!(mk > 0.0f)) y = 0.0f;
+        for (int i = 0; i < 8; ++i) keep[i] = bf16_to_f32((uint16_t)((mk[i >> 1] >> (16 * (i & 1))) & 0xffffu)) > 0.0f;
+      } else {
+        const f32x4 m0 = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(e.mask) + off);
+        const f32x4 m1 = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(e.mask) + off + 4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          keep[i] = m0[i] > 0.0f;
+          keep[i + 4] = m1[i] > 0.0f;
+        }
       }
-      x[i] = y;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      float y = e.alpha * v[i] + bb[i];
+      if (e.relu) y = y > 0.0f ? y : 0.0f;
+      x[i] = keep[i] ? y : 0.0f;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (i < cnt) {
+        float y = e.alpha * v[i] + (e.bias ? e.bias[m + i] : 0.0f);
+        if (e.relu) y = y > 0.0f ? y : 0.0f;
+        if (e.mask) {
+          const int64_t off = (int64_t)n * e.ldmask + m + i;
+          const float mk = e.mask_dtype == IMBD_BF16 ? bf16_to_f32(reinterpret_cast<const uint16_t *>(e.mask)[off])
+                                                     : reinterpret_cast<const float *>(e.mask)[off];
+          if (!(mk > 0.0f)) y = 0.0f;
+        }
+        x[i] = y;
+      }
     }
   }
   if (e.out_dtype == IMBD_BF16) {
@@ -525,7 +559,7 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
   r.aux_scale = p.aux_scale;
   const Epilogue &e = p.epi;
   auto al = [](const void *q, int a) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % a) == 0; };
-  const bool vec = p.M % 8 == 0 && al(e.out, 16) && e.ldo % 8 == 0 &&
+  const bool vec = p.M % 8 == 0 && al(e.out, 16) && e.ldo % 8 == 0 && al(e.bias, 16) &&
                    (e.mask == nullptr || (al(e.mask, 16) && e.ldmask % 8 == 0));
   const int64_t threads = (int64_t)g.tiles_m * p.N * 8;
   const unsigned blocks = (unsigned)((threads + 255) / 256) + (r.aux_loss ? 1u : 0u);
