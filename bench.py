@@ -13,6 +13,7 @@ region's twin) and the CPU oracle timed on a bounded sample of the same workload
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 (--workload conv3x3_tile measures the domain-parallel conv tile instead of the FC step;
 --workload batch_sweep times the FC step at batch sizes 1..2048, --stack alexnet|vgg;
+--workload alexnet_fc_local_4x16 times one process's local blocks of a 4 x 16 grid;
 --workload grid_model times one process's local blocks of the FC stack for every P_r x P_c
 grid of --procs and picks the grid with the cost model of paper_1712_04432_amd.gridmodel)
 """
@@ -357,6 +358,87 @@ def bench_grid_model(args):
     print(json.dumps(out), flush=True)
 
 
+def local_block_bytes(d_out: int, d_in: int, b: int, first: bool) -> int:
+    """Algorithmic bytes of one layer's local forward + backward (bf16 blocks): W_blk read by
+    the forward and (past the first layer) the Delta_X product, the fp32 Delta_W partial
+    written, X_blk read twice (forward, Delta_W), Y_blk (bf16) written, Delta_Y_blk read
+    twice, the fp32 Delta_X partial written and its ReLU mask read."""
+    w = d_out * d_in * (2 + (0 if first else 2) + 4)
+    act = b * d_in * 2 * 2 + b * d_out * 2 + b * d_out * 2 * 2
+    if not first:
+        act += b * d_in * (4 + 2)
+    return w + act
+
+
+def bench_local(args, cfg):
+    """One process's share of the 1.5D grid (the local-block variant): for every layer the
+    local forward (bias + ReLU; the top layer's logits are gathered before softmax, so its
+    block stores them plain) and the local backward (fp32 Delta_W partial, bias partial,
+    masked fp32 Delta_X partial from layer 2 on), on the blocks of a P_r x P_c grid. The
+    partials are left unreduced, as the collectives of Sec. 2.3 would take them."""
+    import numpy as np
+    import torch
+
+    import paper_1712_04432_amd as m
+    from synthdata import make_local_inputs
+
+    m.load()
+    P_r, P_c = cfg.grid
+    b = cfg.batch // P_c
+    dims = cfg.dims
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    L = len(dims) - 1
+    jobs, flops, hbm = [], 0, 0
+    for i in range(1, L + 1):
+        d_out, d_in, first = -(-dims[i] // P_r), dims[i - 1], i == 1
+        d = make_local_inputs(d_out, d_in, b, seed=i)
+        w = torch.from_numpy(d["w_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+        x = torch.from_numpy(d["x_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+        dy = torch.from_numpy(d["dy_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+        bias = torch.from_numpy(d["b"]).to(dev)
+        y = torch.empty(b, d_out, dtype=torch.bfloat16, device=dev)
+        dw = torch.empty(d_out, d_in, device=dev)
+        db = torch.empty(d_out, device=dev)
+        dx = None if first else torch.empty(b, d_in, device=dev)
+        wsz = max(m.mlp_local_workspace_bytes(0, m.IMBD_BF16, d_out, d_in, b),
+                  m.mlp_local_workspace_bytes(1, m.IMBD_BF16, d_out, d_in, b), 16)
+        ws = torch.zeros(wsz, dtype=torch.uint8, device=dev)
+        jobs.append((w, x, dy, bias, y, dw, db, dx, ws, first, i < L))
+        flops += 2 * d_out * d_in * b * (2 if first else 3)
+        hbm += local_block_bytes(d_out, d_in, b, first)
+
+    def step():
+        for w, x, dy, bias, y, dw, db, dx, ws, first, hidden in jobs:
+            m.mlp_local_fwd(w, x, y, P_r, P_c, bias=bias, relu=hidden, ws=ws, stream=stream)
+            m.mlp_local_bwd(w, dy, x, dw, P_r, P_c, db_part=db, dx_part=dx, mask_relu=not first, ws=ws,
+                            stream=stream)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    tflops = flops / (ms * 1e-3) / 1e12
+    t_roof = max(hbm / (PEAK_HBM_GBS * 1e9), flops / (PEAK_BF16_TFLOPS * 1e12)) * 1e3
+    print(json.dumps({
+        "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded N(0,1) blocks, He-initialised weights)",
+        "config": {"workload": f"{cfg.name}: one process's local blocks of the {'-'.join(map(str, dims))} FC stack "
+                               f"on a {P_r}x{P_c} grid, global B = {cfg.batch} (local {b}), forward + backward "
+                               f"partials, unreduced", "global_batch": cfg.batch, "local_batch": b,
+                   "parallelism": f"one process of P_r x P_c = {P_r}x{P_c}"},
+        "samples_per_s": round(b / (ms * 1e-3), 1),
+        "pct_bf16_mfma_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 3), "gflop_per_step": round(flops / 1e9, 4),
+        "algorithmic_hbm_bytes": hbm, "roofline_ms": round(t_roof, 5), "frac_of_roofline": round(t_roof / ms, 4),
+    }), flush=True)
+
+
 def bench_copy(args):
     """A plain device-to-device copy of 512 MiB: the calibration run for the HBM byte
     counters (FETCH_SIZE / WRITE_SIZE per dispatch against the known 512 MiB each way)
@@ -414,8 +496,10 @@ def main():
     import paper_1712_04432_amd as m
     from synthdata import get_config, make_mlp_inputs
 
-    m.load()
     cfg = get_config(args.workload)
+    if tuple(cfg.grid) != (1, 1):
+        return bench_local(args, cfg)
+    m.load()
     dev = torch.device("cuda:0")
     log(f"bench: workload {cfg.name} dims {cfg.dims} B={cfg.batch} dtype={cfg.dtype}")
     d = make_mlp_inputs(cfg, seed=0)

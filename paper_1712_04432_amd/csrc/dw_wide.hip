@@ -253,9 +253,11 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
 }  // namespace
 
 bool dw_wide_fits(const GemmProblem &p) {
-  const char *env = getenv("IMBD_DW_WIDE_MIN_K");  // smallest batch that takes this kernel
-  const int min_k = (env && *env) ? atoi(env) : 257;
   const Epilogue &e = p.epi;
+  // the fused update: batches above 256 (smaller ones run on the persistent kernel); the
+  // fp32 store: any batch
+  const char *env = getenv("IMBD_DW_WIDE_MIN_K");
+  const int min_k = e.mode == EPI_STORE ? 1 : ((env && *env) ? atoi(env) : 257);
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const int64_t lim = (int64_t)1 << 31;  // bytes in one buffer descriptor
   if (p.dtype != IMBD_BF16 || p.a_kc || p.b_kc || e.mask || e.bias || e.relu || p.K < min_k || p.K <= 0 ||

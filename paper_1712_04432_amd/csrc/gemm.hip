@@ -868,6 +868,10 @@ GemmPlan gemm_plan(const GemmProblem &p) {
   if (p.M >= 128 && p.N >= 128) cfg = 1;
   else if (p.M >= 128) cfg = 2;
   else if (p.N >= 128) cfg = 3;
+  const int ktiles = cdiv(p.K, BK);
+  // A short product whose large tiles cannot fill 256 CUs takes 64 x 64 tiles instead
+  // (splitting its few K tiles could not fill them either).
+  if (cfg != 0 && ktiles < 16 && cdiv(p.M, kCfgs[cfg].bm) * cdiv(p.N, kCfgs[cfg].bn) < 256) cfg = 0;
   const int forced = env_int("IMBD_GEMM_CFG", -1);
   if (forced >= 0 && forced < kNumCfgs) cfg = forced;
   pl.cfg = cfg;
@@ -875,12 +879,12 @@ GemmPlan gemm_plan(const GemmProblem &p) {
   pl.bn = kCfgs[cfg].bn;
   const int tiles = cdiv(p.M, pl.bm) * cdiv(p.N, pl.bn);
   // Split K while there are too few tiles to fill 256 CUs twice, keeping >= 4 K tiles
-  // per split; short products are left whole (a second launch would cost more).
+  // per split (>= 2 for products of 4..15 K tiles); a product of fewer K tiles is left
+  // whole (a second launch would cost more).
   int splits = 1;
-  const int ktiles = cdiv(p.K, BK);
-  if (tiles < 512 && ktiles >= 16) {
+  if (tiles < 512 && ktiles >= 4) {
     splits = cdiv(512, tiles);
-    const int max_s = ktiles / 4;
+    const int max_s = ktiles >= 16 ? ktiles / 4 : ktiles / 2;
     if (splits > max_s) splits = max_s;
     if (splits < 1) splits = 1;
   }

@@ -493,7 +493,10 @@ void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
     const double bytes = 2.0 * p.M * p.K + 2.0 * p.N * p.K + 8.0 * s * (double)p.M * p.N;
     const int rounds = (blocks + 255) / 256;
     const double t_cu = rounds * ((ks / SK_KS) * slab_clk + fill_clk) / clk;
-    const double t = bytes / hbm > t_cu ? bytes / hbm : t_cu;
+    // past 16 splits the reduce's threads wait on their loads round after round (four
+    // splits per round): ~0.6 us per extra round
+    const double t_red = 0.6e-6 * (double)((s + 3) / 4 > 4 ? (s + 3) / 4 - 4 : 0);
+    const double t = (bytes / hbm > t_cu ? bytes / hbm : t_cu) + t_red;
     if (forced > 0 ? s == forced : t < best_t * 0.98) {
       best_t = t;
       best_s = s;
