@@ -224,7 +224,7 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const f32x4 g = *reinterpret_cast<const f32x4 *>(stg + (16 * u + sub) * DL_PITCH + 4 * ch);
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a.alpha * g), rw, offw(u), 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a.alpha * g), rw, offw(u), 0, CPOL_COPY_ST);
     }
     return;
   }
