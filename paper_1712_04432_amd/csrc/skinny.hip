@@ -271,41 +271,58 @@ struct SkReduceArgs {
   float aux_scale;
 };
 
-// Adds the splits' partials in split order (the same order and arithmetic as the
-// split-K reduce of the tiled products) and applies the store epilogue:
+// Adds the splits' partials and applies the store epilogue:
 // out(m, n) = [mask(m, n) > 0] * relu?(alpha * sum + bias[m]). Eight consecutive m of one
-// sample per thread; VEC: every access is whole and aligned (checked on the host).
-template <bool VEC>
+// sample per group of LANES threads; VEC: every access is whole and aligned (checked on
+// the host). LANES = 1: one thread adds the splits in split order (the same order and
+// arithmetic as the split-K reduce of the tiled products). LANES = 4 (more than four
+// splits, where one thread would wait on its loads round after round): lane j adds splits
+// j, j+4, j+8, ... in that order, and the four sums are combined as (s0 + s1) + (s2 + s3)
+// by lane exchanges; each exchange adds the same two values on both lanes, so every lane
+// holds the same bits and the result is the same on every run.
+template <bool VEC, int LANES>
 __global__ void __launch_bounds__(256) skinny_reduce(SkReduceArgs g) {
   if (g.aux_loss && blockIdx.x == gridDim.x - 1) {
     __shared__ float part[256];
     block_loss_mean(g.aux_n, g.aux_rows, g.aux_scale, g.aux_loss, part);
     return;
   }
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t tl = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t t = tl / LANES;
+  const int j = (int)(tl - t * LANES);
   const int tile = (int)(t / ((int64_t)g.N * 8));
   const int r = (int)(t - (int64_t)tile * g.N * 8);
   const int n = r >> 3, m = tile * 64 + 8 * (r & 7);
-  if (n >= g.N || m >= g.M) return;
+  if (n >= g.N || m >= g.M) return;  // the same for all LANES lanes of a group
   const Epilogue &e = g.epi;
   const float *p = g.partial + (int64_t)tile * g.tpitch + n * 64 + (m & 63);
-  f32x4 a0 = *reinterpret_cast<const f32x4 *>(p);
-  f32x4 a1 = *reinterpret_cast<const f32x4 *>(p + 4);
-  for (int s0 = 1; s0 < g.splits; s0 += 4) {
+  f32x4 a0 = *reinterpret_cast<const f32x4 *>(p + (int64_t)j * g.sstride);
+  f32x4 a1 = *reinterpret_cast<const f32x4 *>(p + (int64_t)j * g.sstride + 4);
+  for (int s0 = j + LANES; s0 < g.splits; s0 += 4 * LANES) {
     f32x4 q0[4], q1[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      if (s0 + u < g.splits) {
-        const float *q = p + (int64_t)(s0 + u) * g.sstride;
+      if (s0 + u * LANES < g.splits) {
+        const float *q = p + (int64_t)(s0 + u * LANES) * g.sstride;
         q0[u] = *reinterpret_cast<const f32x4 *>(q);
         q1[u] = *reinterpret_cast<const f32x4 *>(q + 4);
       }
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      if (s0 + u < g.splits) {
+      if (s0 + u * LANES < g.splits) {
         a0 += q0[u];
         a1 += q1[u];
       }
+  }
+  if constexpr (LANES > 1) {
+#pragma unroll
+    for (int d = 1; d < LANES; d <<= 1)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a0[i] += __shfl_xor(a0[i], d);
+        a1[i] += __shfl_xor(a1[i], d);
+      }
+    if (j != 0) return;
   }
   const float v[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
   const int cnt = VEC ? 8 : min(8, g.M - m);
@@ -564,12 +581,18 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
   auto al = [](const void *q, int a) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const bool vec = p.M % 8 == 0 && al(e.out, 16) && e.ldo % 8 == 0 && al(e.bias, 16) &&
                    (e.mask == nullptr || (al(e.mask, 16) && e.ldmask % 8 == 0));
-  const int64_t threads = (int64_t)g.tiles_m * p.N * 8;
+  const int lanes = splits > 4 ? 4 : 1;
+  const int64_t threads = (int64_t)g.tiles_m * p.N * 8 * lanes;
   const unsigned blocks = (unsigned)((threads + 255) / 256) + (r.aux_loss ? 1u : 0u);
   {
     LaunchTimer t(IMBD_K_SPLITK, p.layer, s);
-    if (vec) hipLaunchKernelGGL(skinny_reduce<true>, dim3(blocks), dim3(256), 0, s, r);
-    else hipLaunchKernelGGL(skinny_reduce<false>, dim3(blocks), dim3(256), 0, s, r);
+    if (lanes == 4) {
+      if (vec) hipLaunchKernelGGL((skinny_reduce<true, 4>), dim3(blocks), dim3(256), 0, s, r);
+      else hipLaunchKernelGGL((skinny_reduce<false, 4>), dim3(blocks), dim3(256), 0, s, r);
+    } else {
+      if (vec) hipLaunchKernelGGL((skinny_reduce<true, 1>), dim3(blocks), dim3(256), 0, s, r);
+      else hipLaunchKernelGGL((skinny_reduce<false, 1>), dim3(blocks), dim3(256), 0, s, r);
+    }
   }
   return check_launch("skinny_reduce");
 }
