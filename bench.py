@@ -71,8 +71,10 @@ def measured_traffic(workload: str):
 
 def dw_sgd_bytes(d_out: int, d_in: int, batch: int, act_bytes: int = 2) -> int:
     """Algorithmic bytes of one fused weight-gradient + update launch: the fp32 master is
-    read and written, the bf16 copy written (10 B per parameter), X and Delta_Y read once."""
-    return d_out * d_in * (4 + 4 + 2) + batch * (d_in + d_out) * act_bytes
+    read and written, the bf16 copy written (10 B per parameter; 8 B for an fp32 network,
+    whose master is its operand), X and Delta_Y read once."""
+    copy = 2 if act_bytes == 2 else 0
+    return d_out * d_in * (4 + 4 + copy) + batch * (d_in + d_out) * act_bytes
 
 
 def cpu_baseline(cfg, sample_batch: int = 8):
@@ -83,15 +85,17 @@ def cpu_baseline(cfg, sample_batch: int = 8):
     import oracle
     from synthdata import bf16_bits_to_f32, make_mlp_inputs
     d = make_mlp_inputs(cfg, seed=0, batch=sample_batch)
-    xv = bf16_bits_to_f32(d["x_bits"]).astype(np.float64)
+    bf16 = cfg.dtype == "bf16"
+    xv = (bf16_bits_to_f32(d["x_bits"]) if bf16 else d["x"]).astype(np.float64)
     t0 = time.perf_counter()
-    oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, "bf16")
+    oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, "bf16" if bf16 else "f32")
     dt = time.perf_counter() - t0
     flops = cfg.gemm_flops(batch=sample_batch)
     return {"value": round(flops / dt / 1e12, 9), "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle",
             "sample": f"one SGD iteration of the {'-'.join(map(str, cfg.dims))} stack on {sample_batch} of "
-                      f"the {cfg.batch} samples (full weights and update), bf16-mirrored fp64 oracle, "
+                      f"the {cfg.batch} samples (full weights and update), "
+                      f"{'bf16-mirrored' if bf16 else 'fp32-mirrored'} fp64 oracle, "
                       f"{dt:.2f} s = {sample_batch / dt:.3f} samples/s"}
 
 
@@ -504,13 +508,20 @@ def main():
     log(f"bench: workload {cfg.name} dims {cfg.dims} B={cfg.batch} dtype={cfg.dtype}")
     d = make_mlp_inputs(cfg, seed=0)
     net = m.MLP(cfg.dims, cfg.batch, cfg.dtype)
+    bf16 = cfg.dtype == "bf16"
     layers = []
     for w, b in zip(d["w"], d["b"]):
         w32 = torch.from_numpy(w).to(dev)
-        wlp = torch.empty(w.shape, dtype=torch.bfloat16, device=dev)
-        m.cast_f32_bf16(w32, wlp)
+        if bf16:
+            wlp = torch.empty(w.shape, dtype=torch.bfloat16, device=dev)
+            m.cast_f32_bf16(w32, wlp)
+        else:
+            wlp = w32  # an fp32 network computes on its masters
         layers.append({"w": w32, "w_lp": wlp, "b": torch.from_numpy(b).to(dev)})
-    x = torch.from_numpy(d["x_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+    if bf16:
+        x = torch.from_numpy(d["x_bits"].view(np.int16)).to(dev).view(torch.bfloat16)
+    else:
+        x = torch.from_numpy(d["x"]).to(dev)
     lab = torch.from_numpy(d["labels"]).to(dev)
     ws = torch.zeros(m.mlp_workspace_bytes(net), dtype=torch.uint8, device=dev)
     loss = torch.zeros(1, device=dev)
@@ -548,7 +559,8 @@ def main():
     k_avg_ms = k_ms / max(n_launch, 1)
     flops = cfg.gemm_flops()
     tflops = flops / (ms_step * 1e-3) / 1e12
-    dom_bytes = dw_sgd_bytes(cfg.dims[1], cfg.dims[0], cfg.batch)
+    dom_bytes = dw_sgd_bytes(cfg.dims[1], cfg.dims[0], cfg.batch, act_bytes=2 if bf16 else 4)
+    peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
     achieved = dom_bytes / (k_avg_ms * 1e-3) / 1e9
     traffic = measured_traffic(cfg.name)
     result = {
@@ -562,13 +574,16 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1) inputs clamped at 0, uniform labels, He-initialised weights)",
+        "dtype": "bf16" if bf16 else "f32",
+        "data": ("synthetic (seeded N(0,1) inputs clamped at 0, uniform labels, He-initialised weights)" if bf16
+                 else "synthetic (seeded U(0,1) inputs, uniform labels, He-initialised weights)"),
         "config": {"workload": f"{cfg.name}: {'-'.join(map(str, cfg.dims))} FC stack, ReLU, softmax "
-                               f"cross-entropy, bf16 operands / fp32 accumulation / fp32 masters, fused SGD",
+                               f"cross-entropy, " + ("bf16 operands / fp32 accumulation / fp32 masters"
+                                                     if bf16 else "fp32") + ", fused SGD",
                    "global_batch": cfg.batch, "layers": cfg.n_layers, "parallelism": "single GPU (P_r = P_c = 1)"},
         "samples_per_s": round(cfg.batch / (ms_step * 1e-3), 1),
-        "pct_bf16_mfma_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 3),
+        ("pct_bf16_mfma_peak" if bf16 else "pct_fp32_mfma_peak"): round(100.0 * tflops / peak, 3),
+        "us_per_step": round(ms_step * 1e3, 2),
         "gflop_per_step": round(flops / 1e9, 4),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4),
