@@ -110,8 +110,10 @@ void skinny_plan(const GemmProblem &p, int *splits, int *k_split);
 int run_skinny(const GemmProblem &p, void *ws, hipStream_t s);
 size_t skinny_ws_bytes(const GemmProblem &p);
 // Forward / Delta_X products for batches above 256 (bf16, B operand stored [n][k]):
-// whether the large-tile kernel takes the problem, its K split (slabs of 64 per split),
-// and the launch (partials into partial when splits > 1; the caller adds them).
+// whether the large-tile kernel takes the problem (its shapes alone, or with the
+// operands' and output's alignment), its K split (slabs of 64 per split), and the launch
+// (partials into partial when splits > 1; the caller adds them).
+bool wide_shape_fits(const GemmProblem &p);  // the shape conditions alone
 bool wide_fits(const GemmProblem &p);
 void wide_plan(const GemmProblem &p, int *splits, int *kps);
 int run_wide(const GemmProblem &p, float *partial, int64_t ldp, int64_t sstride, hipStream_t s);

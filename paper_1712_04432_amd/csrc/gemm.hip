@@ -26,6 +26,8 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <algorithm>
+
 #include "common.h"
 
 namespace imbd {
@@ -840,27 +842,9 @@ inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 }  // namespace
 
-GemmPlan gemm_plan(const GemmProblem &p) {
+// The tiled template's plan.
+static GemmPlan tiled_plan(const GemmProblem &p) {
   GemmPlan pl{};
-  if (skinny_fits(p) && env_int("IMBD_SKINNY_OFF", 0) == 0) {
-    // the skinny-batch product always goes through fp32 partials (one per K split)
-    skinny_plan(p, &pl.splits, &pl.k_split);
-    pl.cfg = PLAN_SKINNY;
-    pl.bm = 64;
-    pl.bn = 256;
-    pl.ws_bytes = skinny_ws_bytes(p);
-    return pl;
-  }
-  if (wide_fits(p)) {
-    int kps;
-    wide_plan(p, &pl.splits, &kps);
-    pl.cfg = PLAN_WIDE;
-    pl.bm = 256;
-    pl.bn = 128;
-    pl.k_split = 64 * kps;
-    pl.ws_bytes = pl.splits > 1 ? (size_t)pl.splits * (size_t)partial_split_stride(p.M, p.N) * sizeof(float) : 0;
-    return pl;
-  }
   const int esz = p.dtype == IMBD_BF16 ? 2 : 4;
   const int BK = KT_BYTES / esz;
   // Tile: the largest configuration that still gives a reasonable number of tiles.
@@ -896,6 +880,42 @@ GemmPlan gemm_plan(const GemmProblem &p) {
   pl.k_split = k_split;
   pl.ws_bytes = splits > 1 ? (size_t)splits * (size_t)partial_split_stride(p.M, p.N) * sizeof(float) : 0;
   return pl;
+}
+
+GemmPlan gemm_plan(const GemmProblem &p) {
+  // Workspace sizes are computed from the shapes alone, while the skinny and wide kernels
+  // also check their operands' and output's alignment when they run; a run that fails
+  // those checks falls back to the tiled template. So a special kernel's plan asks for
+  // the larger of its own partials and the template's, and any run fits the workspace
+  // that the same shapes were given.
+  const GemmPlan tp = tiled_plan(p);
+  GemmPlan pl{};
+  if (skinny_fits(p) && env_int("IMBD_SKINNY_OFF", 0) == 0) {
+    // the skinny-batch product always goes through fp32 partials (one per K split)
+    skinny_plan(p, &pl.splits, &pl.k_split);
+    pl.cfg = PLAN_SKINNY;
+    pl.bm = 64;
+    pl.bn = 256;
+    pl.ws_bytes = std::max(skinny_ws_bytes(p), tp.ws_bytes);
+    return pl;
+  }
+  if (wide_shape_fits(p)) {
+    int splits, kps;
+    wide_plan(p, &splits, &kps);
+    const size_t wws = splits > 1 ? (size_t)splits * (size_t)partial_split_stride(p.M, p.N) * sizeof(float) : 0;
+    if (wide_fits(p)) {
+      pl.cfg = PLAN_WIDE;
+      pl.bm = 256;
+      pl.bn = 128;
+      pl.splits = splits;
+      pl.k_split = 64 * kps;
+    } else {
+      pl = tp;
+    }
+    pl.ws_bytes = std::max(wws, tp.ws_bytes);
+    return pl;
+  }
+  return tp;
 }
 
 // Adds the split partials in split order and applies the epilogue.

@@ -230,6 +230,27 @@ def test_local_wide_batch_strided_views(imbd, dev):
     assert nrm_err(host(dw), rdw) < 1e-5
 
 
+@pytest.mark.parametrize("b", [64, 300])
+def test_local_fwd_misaligned_block_fits_its_workspace(imbd, dev, b):
+    """A W block whose data starts 2 bytes past a 16-byte boundary fails the skinny (b = 64)
+    and wide-batch (b = 300) kernels' alignment checks and runs on the tiled template; the
+    workspace sized for its shapes alone must still hold that path's partials."""
+    import torch
+    rng = np.random.default_rng(9)
+    dout, din = 264, 1032
+    Wf = rng.standard_normal((dout, din + 8)).astype(np.float32)
+    Xf = rng.standard_normal((b, din)).astype(np.float32)
+    Wb, Xb = to_bf16_bits(Wf), to_bf16_bits(Xf)
+    wd, xd = dev_bf16_bits(Wb, dev), dev_bf16_bits(Xb, dev)
+    wblk = wd[:, 1:din + 1]                       # leading dimension din + 8, data 2 bytes off
+    assert wblk.data_ptr() % 16 == 2
+    y = torch.empty((b, dout), device=dev)
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(0, 1, dout, din, b), 16), dtype=torch.uint8, device=dev)
+    imbd.mlp_local_fwd(wblk, xd, y, 1, 1, ws=ws)
+    ref = oracle.affine_fwd(bf16_values(Wb)[:, 1:din + 1], bf16_values(Xb))
+    assert nrm_err(host(y), ref) < 1e-5
+
+
 def test_local_bwd_empty_block_writes_zero_partials(imbd, dev):
     import torch
     dw = torch.full((5, 7), 3.0, device=dev)
