@@ -430,6 +430,8 @@ static GemmProblem local_fwd_problem(int dtype, int d_out_blk, int d_in, int b_b
   p.N = b_blk;
   p.K = d_in;
   p.a_kc = p.b_kc = true;
+  p.lda = d_in;  // contiguous blocks; the caller's leading dimensions replace these
+  p.ldb = d_in;
   p.kclass = IMBD_K_GEMM_FWD;
   return p;
 }
@@ -440,6 +442,8 @@ static GemmProblem local_dw_problem(int dtype, int d_out_blk, int d_in, int b_bl
   p.N = d_out_blk;
   p.K = b_blk;
   p.a_kc = p.b_kc = false;
+  p.lda = d_in;
+  p.ldb = d_out_blk;
   p.kclass = IMBD_K_GEMM_DW;
   return p;
 }
@@ -451,6 +455,8 @@ static GemmProblem local_dx_problem(int dtype, int d_out_blk, int d_in, int b_bl
   p.K = d_out_blk;
   p.a_kc = false;
   p.b_kc = true;
+  p.lda = d_in;
+  p.ldb = d_out_blk;
   p.kclass = IMBD_K_GEMM_DX;
   return p;
 }

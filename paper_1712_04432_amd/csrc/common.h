@@ -105,15 +105,16 @@ inline int64_t partial_split_stride(int M, int N) { return (int64_t)N * partial_
 // Forward / Delta_X products for batches up to 256 (bf16): whether the skinny kernel
 // takes the problem, its K split, the launch (kernel + its reduce) and the bytes of
 // partial sums it needs in ws.
+bool skinny_dims_fit(const GemmProblem &p);  // the conditions on M, N, K, dtype and epilogue mode
 bool skinny_fits(const GemmProblem &p);
 void skinny_plan(const GemmProblem &p, int *splits, int *k_split);
 int run_skinny(const GemmProblem &p, void *ws, hipStream_t s);
 size_t skinny_ws_bytes(const GemmProblem &p);
 // Forward / Delta_X products for batches above 256 (bf16, B operand stored [n][k]):
-// whether the large-tile kernel takes the problem (its shapes alone, or with the
-// operands' and output's alignment), its K split (slabs of 64 per split), and the launch
+// whether the large-tile kernel takes the problem (its dimensions alone, or with the
+// leading dimensions and the operands' and output's alignment), its K split (slabs of 64 per split), and the launch
 // (partials into partial when splits > 1; the caller adds them).
-bool wide_shape_fits(const GemmProblem &p);  // the shape conditions alone
+bool wide_dims_fit(const GemmProblem &p);  // the conditions on M, N, K, dtype and epilogue mode
 bool wide_fits(const GemmProblem &p);
 void wide_plan(const GemmProblem &p, int *splits, int *kps);
 int run_wide(const GemmProblem &p, float *partial, int64_t ldp, int64_t sstride, hipStream_t s);

@@ -883,23 +883,27 @@ static GemmPlan tiled_plan(const GemmProblem &p) {
 }
 
 GemmPlan gemm_plan(const GemmProblem &p) {
-  // Workspace sizes are computed from the shapes alone, while the skinny and wide kernels
-  // also check their operands' and output's alignment when they run; a run that fails
-  // those checks falls back to the tiled template. So a special kernel's plan asks for
-  // the larger of its own partials and the template's, and any run fits the workspace
-  // that the same shapes were given.
+  // Workspace sizes are computed from the dimensions alone, while the skinny and wide
+  // kernels also check leading dimensions and alignment when they run; a run that fails
+  // those checks falls back to the tiled template. So a plan whose dimensions admit a
+  // special kernel asks for the larger of that kernel's partials and the template's, and
+  // any run fits the workspace that the same dimensions were given.
   const GemmPlan tp = tiled_plan(p);
   GemmPlan pl{};
-  if (skinny_fits(p) && env_int("IMBD_SKINNY_OFF", 0) == 0) {
-    // the skinny-batch product always goes through fp32 partials (one per K split)
-    skinny_plan(p, &pl.splits, &pl.k_split);
-    pl.cfg = PLAN_SKINNY;
-    pl.bm = 64;
-    pl.bn = 256;
+  if (skinny_dims_fit(p) && env_int("IMBD_SKINNY_OFF", 0) == 0) {
+    if (skinny_fits(p)) {
+      // the skinny-batch product always goes through fp32 partials (one per K split)
+      skinny_plan(p, &pl.splits, &pl.k_split);
+      pl.cfg = PLAN_SKINNY;
+      pl.bm = 64;
+      pl.bn = 256;
+    } else {
+      pl = tp;
+    }
     pl.ws_bytes = std::max(skinny_ws_bytes(p), tp.ws_bytes);
     return pl;
   }
-  if (wide_shape_fits(p)) {
+  if (wide_dims_fit(p)) {
     int splits, kps;
     wide_plan(p, &splits, &kps);
     const size_t wws = splits > 1 ? (size_t)splits * (size_t)partial_split_stride(p.M, p.N) * sizeof(float) : 0;

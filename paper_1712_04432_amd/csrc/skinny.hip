@@ -479,13 +479,17 @@ int env_splits() { return env_int_skinny("IMBD_SKINNY_SPLITS"); }
 
 }  // namespace
 
+bool skinny_dims_fit(const GemmProblem &p) {
+  return p.dtype == IMBD_BF16 && p.b_kc && p.epi.mode == EPI_STORE && p.db_mode == 0 && p.N >= 1 &&
+         p.N <= 256 && p.M >= 1 && p.K >= 8 && p.K % 8 == 0 && (p.a_kc || p.M % 8 == 0);
+}
+
 bool skinny_fits(const GemmProblem &p) {
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const int64_t arows = p.a_kc ? p.M : p.K;
-  return p.dtype == IMBD_BF16 && p.b_kc && p.epi.mode == EPI_STORE && p.db_mode == 0 && p.N >= 1 &&
-         p.N <= 256 && p.M >= 1 && p.K >= 8 && p.K % 8 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
-         al(p.A, 16) && al(p.B, 16) && (arows + SK_KS + SK_BM) * p.lda * 2 < ((int64_t)1 << 31) &&
-         ((int64_t)256 * p.ldb + p.K + SK_KS) * 2 < ((int64_t)1 << 31) && (p.a_kc || p.M % 8 == 0);
+  return skinny_dims_fit(p) && p.lda % 8 == 0 && p.ldb % 8 == 0 && al(p.A, 16) && al(p.B, 16) &&
+         (arows + SK_KS + SK_BM) * p.lda * 2 < ((int64_t)1 << 31) &&
+         ((int64_t)256 * p.ldb + p.K + SK_KS) * 2 < ((int64_t)1 << 31);
 }
 
 // Splits: fill the chip, traded against the partials' traffic (each split writes an

@@ -333,23 +333,22 @@ int64_t a_extent(const GemmProblem &p) {
 
 }  // namespace
 
-bool wide_shape_fits(const GemmProblem &p) {
+bool wide_dims_fit(const GemmProblem &p) {
   const char *env = getenv("IMBD_WIDE_OFF");  // 1: use the tiled GEMM template instead
   if (env && atoi(env) != 0) return false;
-  if (p.dtype != IMBD_BF16 || !p.b_kc || p.db_mode != 0 || p.epi.mode != EPI_STORE) return false;
-  if (p.M < 128 || p.N <= 256 || p.K < WD_KS) return false;
-  if (p.M % 8 || p.K % 8 || p.lda % 8 || p.ldb % 8) return false;
-  if (p.a_kc ? p.lda < p.K : p.lda < p.M) return false;
-  if (p.ldb < p.K) return false;
-  const int64_t lim = (int64_t)1 << 30;  // elements: 2 GiB of bf16 in a buffer descriptor
-  return a_extent(p) < lim && (int64_t)(p.N - 1) * p.ldb + p.K < lim &&
-         (int64_t)p.N * partial_ld(p.M) < lim / 2;  // partial rows in one descriptor
+  return p.dtype == IMBD_BF16 && p.b_kc && p.db_mode == 0 && p.epi.mode == EPI_STORE && p.M >= 128 &&
+         p.N > 256 && p.K >= WD_KS && p.M % 8 == 0 && p.K % 8 == 0;
 }
 
 bool wide_fits(const GemmProblem &p) {
   auto al = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) % 16) == 0; };
   const Epilogue &e = p.epi;
-  if (!wide_shape_fits(p) || !al(p.A) || !al(p.B)) return false;
+  if (!wide_dims_fit(p) || p.lda % 8 || p.ldb % 8 || !al(p.A) || !al(p.B)) return false;
+  if (p.a_kc ? p.lda < p.K : p.lda < p.M) return false;
+  if (p.ldb < p.K) return false;
+  const int64_t lim = (int64_t)1 << 30;  // elements: 2 GiB of bf16 in a buffer descriptor
+  if (a_extent(p) >= lim || (int64_t)(p.N - 1) * p.ldb + p.K >= lim || (int64_t)p.N * partial_ld(p.M) >= lim / 2)
+    return false;
   if (!e.out || e.ldo % 8 || !al(e.out) || (e.bias && !al(e.bias))) return false;
   return !e.mask || (e.mask_dtype == IMBD_BF16 && e.ldmask % 8 == 0 && al(e.mask));
 }
