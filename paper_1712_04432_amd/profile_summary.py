@@ -1,6 +1,8 @@
 """Summarise a rocprofv3 kernel trace (CSV) per kernel and launch shape.
 
 Usage: python -m paper_1712_04432_amd.profile_summary <..._kernel_trace.csv> [--title TEXT]
+       python -m paper_1712_04432_amd.profile_summary <run_counter_collection.csv> --counter NAME --kernel SUBSTR
+       python -m paper_1712_04432_amd.profile_summary <run_counter_collection.csv> --mfma
 
 rocprofv3's own --stats groups launches by kernel symbol only; the weight-gradient
 kernel of every layer is one symbol, so this groups by (symbol, grid size) as well and
@@ -62,6 +64,37 @@ def counter_per_dispatch(path: str, kernel: str, counter: str):
     return [tot[d] for d in sorted(tot)]
 
 
+def mfma_utilisation(path: str, simds: int = 1024, xcds: int = 8):
+    """Per (kernel, grid) of a --pmc run with SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE:
+    the matrix-pipe utilisation MFMA_BUSY / (cycles x SIMDs), MFMA_BUSY counting the busy
+    cycles of every SIMD's matrix pipe (16 per 16x16x32 bf16 MFMA). Two cycle counts:
+    GRBM_GUI_ACTIVE per XCD (it is summed over the XCDs; the measured clock, but its
+    window also covers the dispatch's launch and drain, which inflates it for launches of
+    a few microseconds), and the dispatch's duration at the 2.4 GHz peak clock (the share
+    of the dense peak). Medians over the dispatches of each group."""
+    disp = collections.OrderedDict()
+    for r in csv.DictReader(open(path)):
+        d = int(r["Dispatch_Id"])
+        e = disp.setdefault(d, {"name": short_name(r["Kernel_Name"]), "grid": int(r["Grid_Size"]),
+                                "wg": int(r["Workgroup_Size"]),
+                                "dur": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    groups = collections.defaultdict(list)
+    for e in disp.values():
+        if e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) > 0 and e.get("GRBM_GUI_ACTIVE", 0.0) > 0:
+            cyc = e["GRBM_GUI_ACTIVE"] / xcds
+            groups[(e["name"], e["grid"] // max(e["wg"], 1), e["wg"])].append(
+                (e["dur"], cyc / e["dur"] / 1e3, e["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * simds),
+                 e["SQ_VALU_MFMA_BUSY_CYCLES"] / (e["dur"] * 2.4e3 * simds)))
+    out = []
+    for (name, grid, wg), v in groups.items():
+        out.append({"kernel": name, "workgroups": grid, "wg_size": wg, "dispatches": len(v),
+                    "dur_us": statistics.median(x[0] for x in v), "clock_ghz": statistics.median(x[1] for x in v),
+                    "mfma_util": statistics.median(x[2] for x in v),
+                    "mfma_peak": statistics.median(x[3] for x in v)})
+    return sorted(out, key=lambda r: -r["dur_us"] * r["dispatches"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("trace")
@@ -72,7 +105,18 @@ def main():
     ap.add_argument("--per-step-ref", default="", help="kernel launched once per step (splits layers)")
     ap.add_argument("--period", type=int, default=1,
                     help="dispatches of the kernel per step; one median per position in the step")
+    ap.add_argument("--mfma", action="store_true",
+                    help="matrix-pipe utilisation per kernel of a --pmc run with SQ_VALU_MFMA_BUSY_CYCLES "
+                         "and GRBM_GUI_ACTIVE")
     a = ap.parse_args()
+    if a.mfma:
+        print("| kernel | workgroups x size | dispatches | median us | GUI clock GHz | MFMA busy of GUI cycles | "
+              "MFMA busy at 2.4 GHz |")
+        print("|---|---|---|---|---|---|---|")
+        for r in mfma_utilisation(a.trace)[:a.top]:
+            print(f"| `{r['kernel']}` | {r['workgroups']} x {r['wg_size']} | {r['dispatches']} | {r['dur_us']:.2f} | "
+                  f"{r['clock_ghz']:.2f} | {100 * r['mfma_util']:.1f}% | {100 * r['mfma_peak']:.1f}% |")
+        return
     if a.counter:
         v = counter_per_dispatch(a.trace, a.kernel, a.counter)
         print(f"{a.counter} per dispatch of '{a.kernel}' ({len(v)} dispatches)")
