@@ -3,8 +3,6 @@
 // conversion of master weights. Wave64 throughout; every reduction runs in a fixed order
 // so repeated calls give identical bits.
 
-#include <stdlib.h>
-
 #include "common.h"
 #include "loss_mean.h"
 
@@ -121,26 +119,22 @@ __global__ void __launch_bounds__(256)
   }
 }
 
-// The same column sums for bf16 Delta_Y with 16-byte row chunks (8 columns): CH chunks
-// (8*CH columns) per workgroup, thread t sums chunk t%CH over the rows r = t/CH + (256/CH)i in
-// ascending order (eight loads in flight per batch), then the 256/CH row phases are added in
-// phase order. Fewer columns per workgroup give more workgroups for the same rows (the sums
-// are latency-bound at a few MB).
-template <int CH>
+// The same column sums for bf16 Delta_Y with 16-byte rows chunks (8 columns): 64 columns per
+// workgroup, thread t sums chunk t%8 over the rows r = t/8 + 32i in ascending order (eight
+// loads in flight per batch), then the 32 row phases are added in phase order.
 __global__ void __launch_bounds__(256)
     bias_grad_wide(int M, int B, const uint16_t *__restrict__ dy, int64_t lddy, float alpha,
                    float *__restrict__ db_out, float *__restrict__ bias, float lr) {
-  constexpr int PH = 256 / CH, COLS = 8 * CH;
-  __shared__ float part[PH][COLS + 4];
-  const int j = threadIdx.x % CH, q = threadIdx.x / CH;
-  const int m0 = blockIdx.x * COLS + 8 * j;
+  __shared__ float part[32][64 + 4];
+  const int j = threadIdx.x & 7, q = threadIdx.x >> 3;
+  const int m0 = blockIdx.x * 64 + 8 * j;
   const bool live = m0 < M;  // M % 8 == 0: a chunk is wholly in or out
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int r0 = q; r0 < B; r0 += PH * 8) {
+  for (int r0 = q; r0 < B; r0 += 32 * 8) {
     u32x4 v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int r = r0 + PH * u;
+      const int r = r0 + 32 * u;
       v[u] = live && r < B ? *reinterpret_cast<const u32x4 *>(dy + (int64_t)r * lddy + m0) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
@@ -154,10 +148,10 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
   for (int e = 0; e < 8; ++e) part[q][8 * j + e] = s[e];
   __syncthreads();
-  if (threadIdx.x < COLS) {
-    const int m = blockIdx.x * COLS + threadIdx.x;
+  if (threadIdx.x < 64) {
+    const int m = blockIdx.x * 64 + threadIdx.x;
     float t = 0.f;
-    for (int k = 0; k < PH; ++k) t += part[k][threadIdx.x];
+    for (int k = 0; k < 32; ++k) t += part[k][threadIdx.x];
     if (m < M) {
       const float g = alpha * t;
       if (db_out) db_out[m] = g;
@@ -254,21 +248,9 @@ int run_bias_grad(int dtype, int M, int B, const void *dy, int64_t lddy, float a
                   float *db_out, float *bias_sgd, float lr, hipStream_t s, int layer) {
   if (M <= 0) return IMBD_OK;
   LaunchTimer t(IMBD_K_BIAS, layer, s);
-  if (dtype == IMBD_BF16 && M % 8 == 0 && lddy % 8 == 0 && (uintptr_t)dy % 16 == 0) {
-    // 32 columns per workgroup: against 64, the VGG step (B = 512) 7 us faster, the others
-    // unchanged; 16 was slower at B = 2048
-    const char *env = getenv("IMBD_BIAS_CH");
-    const int ch = env && *env ? atoi(env) : 4;
-    if (ch == 2)
-      hipLaunchKernelGGL(bias_grad_wide<2>, dim3((M + 15) / 16), dim3(256), 0, s, M, B,
-                         reinterpret_cast<const uint16_t *>(dy), lddy, alpha, db_out, bias_sgd, lr);
-    else if (ch == 4)
-      hipLaunchKernelGGL(bias_grad_wide<4>, dim3((M + 31) / 32), dim3(256), 0, s, M, B,
-                         reinterpret_cast<const uint16_t *>(dy), lddy, alpha, db_out, bias_sgd, lr);
-    else
-      hipLaunchKernelGGL(bias_grad_wide<8>, dim3((M + 63) / 64), dim3(256), 0, s, M, B,
-                         reinterpret_cast<const uint16_t *>(dy), lddy, alpha, db_out, bias_sgd, lr);
-  }
+  if (dtype == IMBD_BF16 && M % 8 == 0 && lddy % 8 == 0 && (uintptr_t)dy % 16 == 0)
+    hipLaunchKernelGGL(bias_grad_wide, dim3((M + 63) / 64), dim3(256), 0, s, M, B,
+                       reinterpret_cast<const uint16_t *>(dy), lddy, alpha, db_out, bias_sgd, lr);
   else if (dtype == IMBD_BF16)
     hipLaunchKernelGGL(bias_grad_kernel<uint16_t>, dim3((M + 63) / 64), dim3(256), 0, s, M, B,
                        reinterpret_cast<const uint16_t *>(dy), lddy, alpha, db_out, bias_sgd, lr);
