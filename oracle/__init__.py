@@ -23,7 +23,7 @@ Precision modes of :func:`train_step`:
 ``"f32"``
     the same storage points rounded to binary32 (the fp32 device path).
 
-Readings of the paper used here (each also listed in the design doc):
+Readings of the paper used here, where it is silent or ambiguous:
 
 * The mean 1/B of Eq. (1) is folded into the top-layer gradient, so every lower
   gradient is already the mini-batch mean; B is a power of two in every workload, so

@@ -4,8 +4,8 @@ batch and pure model costs at the ends of the grid range and the integrated mode
 domain cost to the 1.5D cost without domain layers (Sec. 2.3, Sec. 2.4); the redistribution
 is a third of a model-parallel layer's traffic (Sec. 2.2); the batch/model volume ratio of
 the AlexNet 3x3 convolution on 13x13x384 activations crosses 1 between B = 13 and 14 (the
-paper says model parallelism wins for B <= 12; its own formula gives B < 13.6, a reading
-recorded in the design doc); the weight all-reduce volume falls by P_r; and the selector returns
+paper says model parallelism wins for B <= 12; its own formula gives B < 13.6, and the
+formula is what is pinned); the weight all-reduce volume falls by P_r; and the selector returns
 the brute-force minimum."""
 import math
 

@@ -268,7 +268,8 @@ def test_grid_detects_a_missing_process():
 
 def test_grid_simulation_of_a_whole_network_step():
     """Run every layer of a 3-layer step through the software grid and compare with the
-    unpartitioned step (softmax on the gathered logits, as the reading in the design doc)."""
+    unpartitioned step (the top layer's softmax on the gathered logits: softmax needs whole
+    columns, so each process slices its rows of the gradient afterwards)."""
     cfg = scaled_mlp((24, 16, 16, 8), 8, "f32", x_dist="normal")
     d = make_mlp_inputs(cfg, seed=12)
     ref = oracle.train_step(d["w"], d["b"], d["x"], d["labels"], 0.01)
