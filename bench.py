@@ -77,26 +77,34 @@ def dw_sgd_bytes(d_out: int, d_in: int, batch: int, act_bytes: int = 2) -> int:
     return d_out * d_in * (4 + 4 + copy) + batch * (d_in + d_out) * act_bytes
 
 
-def cpu_baseline(cfg, sample_batch: int = 8):
-    """The oracle, as it is, on one SGD iteration of the same network restricted to
-    `sample_batch` samples (the full weights and update are still processed)."""
+def cpu_baseline(cfg, sample_batch: int = 0, min_seconds: float = 10.0):
+    """The oracle, as it is, on SGD iterations of the same network over `sample_batch`
+    samples (0: the whole batch; the full weights and update are processed either way),
+    repeated until `min_seconds` have passed; the rate is over all iterations."""
     import numpy as np
 
     import oracle
     from synthdata import bf16_bits_to_f32, make_mlp_inputs
-    d = make_mlp_inputs(cfg, seed=0, batch=sample_batch)
+    n = sample_batch or cfg.batch
+    d = make_mlp_inputs(cfg, seed=0, batch=n)
     bf16 = cfg.dtype == "bf16"
     xv = (bf16_bits_to_f32(d["x_bits"]) if bf16 else d["x"]).astype(np.float64)
+    iters = 0
     t0 = time.perf_counter()
-    oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, "bf16" if bf16 else "f32")
-    dt = time.perf_counter() - t0
-    flops = cfg.gemm_flops(batch=sample_batch)
+    while True:
+        oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, "bf16" if bf16 else "f32")
+        iters += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    flops = iters * cfg.gemm_flops(batch=n)
+    whole = "all" if n == cfg.batch else f"{n} of the"
     return {"value": round(flops / dt / 1e12, 9), "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle",
-            "sample": f"one SGD iteration of the {'-'.join(map(str, cfg.dims))} stack on {sample_batch} of "
-                      f"the {cfg.batch} samples (full weights and update), "
+            "sample": f"{iters} SGD iteration(s) of the {'-'.join(map(str, cfg.dims))} stack on {whole} "
+                      f"{cfg.batch} samples (full weights and update), "
                       f"{'bf16-mirrored' if bf16 else 'fp32-mirrored'} fp64 oracle, "
-                      f"{dt:.2f} s = {sample_batch / dt:.3f} samples/s"}
+                      f"{dt:.2f} s = {iters * n / dt:.3f} samples/s"}
 
 
 def conv_cpu_baseline(cfg, images: int = 8):
@@ -474,7 +482,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="alexnet_fc_b256")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-batch", type=int, default=8)
+    ap.add_argument("--cpu-sample-batch", type=int, default=0, help="samples in the oracle's timed step (0: the whole batch)")
     ap.add_argument("--stack", default="alexnet", choices=("alexnet", "vgg"))
     ap.add_argument("--batches", default="1,2,4,8,16,32,64,128,256,512,1024,2048")
     ap.add_argument("--procs", default="8,64,512")

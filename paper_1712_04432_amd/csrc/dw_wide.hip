@@ -1,4 +1,4 @@
-// Fused weight gradient + SGD update of a fully connected layer for batches above 256
+// Fused weight gradient + SGD update of a fully connected layer for batches above 384
 // samples (bf16 operands, fp32 masters):
 //   Delta_W[o][i] = sum_b Delta_Y[b][o] X[b][i]      (Sec. 1, K = the batch)
 //   w[o][i] -= lr * alpha * Delta_W[o][i];  w16[o][i] = bf16(w[o][i])   (Eq. (1))
@@ -254,10 +254,11 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
 
 bool dw_wide_fits(const GemmProblem &p) {
   const Epilogue &e = p.epi;
-  // the fused update: batches above 256 (smaller ones run on the persistent kernel); the
-  // fp32 store: any batch
+  // the fused update: batches above 384 (smaller ones run on the persistent kernel, which
+  // streams Delta_Y past 256 samples and is the faster of the two up to 384 on the AlexNet
+  // and VGG FC stacks); the fp32 store: any batch
   const char *env = getenv("IMBD_DW_WIDE_MIN_K");
-  const int min_k = e.mode == EPI_STORE ? 1 : ((env && *env) ? atoi(env) : 257);
+  const int min_k = e.mode == EPI_STORE ? 1 : ((env && *env) ? atoi(env) : 385);
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const int64_t lim = (int64_t)1 << 31;  // bytes in one buffer descriptor
   if (p.dtype != IMBD_BF16 || p.a_kc || p.b_kc || e.mask || e.bias || e.relu || p.K < min_k || p.K <= 0 ||

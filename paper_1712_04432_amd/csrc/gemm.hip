@@ -1021,8 +1021,9 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     if (rc == IMBD_OK && pl.splits > 1) rc = launch_reduce(p, g, s);
     return rc;
   }
-  // A bf16 weight gradient past 256 samples runs on the large-tile kernel (fused update or
-  // fp32 store); the fused update of a smaller batch on the persistent one.
+  // A bf16 weight gradient runs on the large-tile kernel when stored as fp32 (any batch) or
+  // fused with the update past 384 samples; the fused update of a smaller batch on the
+  // persistent one.
   if (dw_wide_fits(p)) return run_dw_wide(p, s);
   if (dw_sgd_fits(p) && env_int("IMBD_DW_GENERIC", 0) == 0) return run_dw_sgd(p, s);
   const TileCfg &c = kCfgs[pl.cfg];

@@ -103,13 +103,35 @@ def test_bf16_one_step_matches_mirrored_oracle(imbd, dev, dims, B):
 
 @pytest.mark.parametrize("dims,B", [((2056, 2104, 24), 72), ((136, 8, 16), 8), ((4096, 1000, 128), 256),
                                     ((136, 8, 16), 1), ((264, 128, 24), 5),
-                                    # past 256 samples the Delta_Y block is reloaded per 256-sample chunk
+                                    # past 256 samples: Delta_Y streamed (300), large tiles (777)
                                     ((264, 128, 24), 300), ((1032, 264, 16), 777)])
 def test_bf16_fused_update_matches_oracle(imbd, dev, dims, B):
     """The fused weight update (Eq. (1) applied inside the weight-gradient product) on
     shapes that give the persistent update kernel several tiles per workgroup (17 x 17
     tiles of the first layer), ragged tile edges and a batch that is not a multiple of
     the 64-sample K tile; the bf16 copy must be the rounding of every new master."""
+    _check_fused_update(imbd, dev, dims, B)
+
+
+# the switches that route the fused update past 256 samples (read at every launch)
+_UPDATE_ROUTES = {"streamed": {"IMBD_DW_WIDE_MIN_K": "100000"},
+                  "reload": {"IMBD_DW_WIDE_MIN_K": "100000", "IMBD_DW_STREAM": "0"},
+                  "wide": {"IMBD_DW_WIDE_MIN_K": "257"}}
+
+
+@pytest.mark.parametrize("route", sorted(_UPDATE_ROUTES))
+@pytest.mark.parametrize("dims,B", [((264, 128, 24), 300), ((1032, 264, 16), 777), ((2056, 520, 16), 2048)])
+def test_bf16_fused_update_every_kernel_past_256_samples(imbd, dev, monkeypatch, dims, B, route):
+    """Past 256 samples three kernels can apply the fused update: the persistent one with
+    Delta_Y streamed in slabs (the default up to 384 samples), the persistent one with its
+    resident Delta_Y block reloaded per 256-sample chunk, and the large-tile one (the
+    default past 384). Each is forced in turn, up to the persistent kernel's 2048 samples."""
+    for k, v in _UPDATE_ROUTES[route].items():
+        monkeypatch.setenv(k, v)
+    _check_fused_update(imbd, dev, dims, B)
+
+
+def _check_fused_update(imbd, dev, dims, B):
     import torch
     cfg = scaled_mlp(dims, B, "bf16")
     _flush(f"bf16 fused update {dims} B={B}")
@@ -183,10 +205,11 @@ def test_train_step_loss_equals_forward_loss(imbd, dev, dims, B):
     assert abs(loss.item() - ref["loss"]) < TOL_BF16 * abs(ref["loss"])
 
 
-@pytest.mark.parametrize("B", [128, 600])
+@pytest.mark.parametrize("B", [128, 300, 600])
 def test_step_is_deterministic(imbd, dev, B):
     """Two identical steps give identical bits (fixed split order in every reduction),
-    also past 256 samples where the update reloads its Delta_Y block per chunk."""
+    also past 256 samples: Delta_Y streamed through the update kernel (300), the large-tile
+    products (600)."""
     import torch
     cfg = scaled_mlp((2048, 512, 256, 100), B, "bf16")
     outs = []
