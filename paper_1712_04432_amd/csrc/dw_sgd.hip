@@ -62,6 +62,7 @@ struct DwArgs {
   float *db_out, *bias;
   float db_alpha, bias_lr;
   int tiles_m, tiles_n;
+  int spread;          // row-block order (see the kernel)
 };
 
 // STREAM (batches past 256): Delta_Y travels in 32-sample slabs through a ring of its own,
@@ -91,7 +92,12 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
   // The gpb workgroups of a column block share its row blocks; the k-th row block of the
   // one with index grp is gpb*k + (grp + k) % gpb, so that every workgroup visits every
   // column offset modulo gpb row blocks. (A fixed offset per workgroup left some of them
-  // on slow address classes: layer-1 finish times spread 53-73 us, now 62-70 us.)
+  // on slow address classes: layer-1 finish times spread 53-73 us, now 62-70 us.) The gpb
+  // row blocks in flight at once are then adjacent, one 4 KB run of each master row; when
+  // the row pitch is a multiple of 8 KB those runs fall in at most two of the four 4 KB
+  // pages modulo 16 KB, and the update streams slower (4096 x 4096: 41 us). With spread
+  // set, the k-th row block is full*((grp + k) % gpb) + k instead: the blocks in flight
+  // are full blocks apart (34 us). The rem extra blocks come last either way.
   const int gpb = G / a.tiles_n, grp = b / a.tiles_n;
   const int full = a.tiles_m / gpb, rem = a.tiles_m % gpb;
   const int nmy = b < tiles ? full + ((grp + full) % gpb < rem ? 1 : 0) : 0;
@@ -103,7 +109,10 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
   const bool multi = !STREAM && nch > 1;
   auto reloads = [&](int it) { return multi ? nch - (it == nmy - 1 ? 1 : 0) : 0; };
   const int n0 = (b % a.tiles_n) * BN;
-  auto tile_m0 = [&](int it) { return (gpb * it + (grp + it) % gpb) * BM; };
+  auto tile_m0 = [&](int it) {
+    const int r = (grp + it) % gpb;
+    return (it < full && a.spread ? r * full + it : gpb * it + r) * BM;
+  };
 
   if (tid < NTM) {
     // ------------------------------------------------------------------ MMA group
@@ -452,6 +461,7 @@ int run_dw_sgd(const GemmProblem &p, hipStream_t s) {
   d.bias_lr = p.bias_lr;
   d.tiles_m = (p.M + 127) / 128;
   d.tiles_n = (p.N + 127) / 128;
+  d.spread = (p.epi.ldo * 4) % 8192 == 0;
   // past 256 samples Delta_Y streams in slabs beside X (IMBD_DW_STREAM=0: the resident
   // block reloaded per 256-sample chunk instead)
   const char *env = getenv("IMBD_DW_STREAM");
