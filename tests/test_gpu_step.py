@@ -103,6 +103,8 @@ def test_bf16_one_step_matches_mirrored_oracle(imbd, dev, dims, B):
 
 @pytest.mark.parametrize("dims,B", [((2056, 2104, 24), 72), ((136, 8, 16), 8), ((4096, 1000, 128), 256),
                                     ((136, 8, 16), 1), ((264, 128, 24), 5),
+                                    # 16 KB master pitch, two tiles per workgroup: the spread row-block order
+                                    ((4096, 2048, 16), 72),
                                     # past 256 samples: Delta_Y streamed (300), large tiles (777)
                                     ((264, 128, 24), 300), ((1032, 264, 16), 777)])
 def test_bf16_fused_update_matches_oracle(imbd, dev, dims, B):
