@@ -26,6 +26,8 @@
 #include <hip/hip_ext.h>
 #include <stdlib.h>
 
+#include <type_traits>
+
 #include "cdna4.h"
 
 namespace imbd {
@@ -355,11 +357,16 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
     // A master vector is loaded CHUNKS - LAG chunks (slab barriers) before the pass that
     // needs it: far enough ahead to cover the HBM latency, near enough that the CU's queue
     // of outstanding requests stays short and the operand loads are not stuck behind it.
+    // The first two iterations are peeled (PH 0 and 1, the rest PH 2) so that tile 0's
+    // masters are all loaded during its product, chunk ch at chunk ch of iteration 0, with
+    // no conditional load in any iteration: iteration 0 stores nothing, iteration 1 skips
+    // the loads of tile 0's second half, which are already in the registers.
     constexpr int LAG = 4;
     f32x4 wold[PASSES];
     int pm0 = 0;
     lds_barrier();  // matches the MMA group's "Delta_Y block and slab 0 landed"
-    for (int it = 0; it <= nmy; ++it) {
+    auto iteration = [&](auto phase, int it) {
+      constexpr int PH = decltype(phase)::value;
       const bool have = it < nmy;
       const int m0 = have ? tile_m0(it) : 0;
       // rn: tile it (masters for passes loaded late in this iteration), rq: tile it-1
@@ -380,6 +387,7 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
       for (int ch = 0; ch < CHUNKS; ++ch) {
 #pragma unroll
         for (int q = 0; q < CP; ++q) {
+          if constexpr (PH == 0) break;  // no tile before tile 0
           const int pp = ch * CP + q;
           const f32x4 v = *(const __attribute__((address_space(3))) f32x4 *)(uintptr_t)(sb[pp & 3] + pp * RPP * BM * 4);
           f32x4 nw;
@@ -394,10 +402,13 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
         // refill the registers of chunk ch - LAG (tile it) or ch - LAG + CHUNKS (tile it-1)
 #pragma unroll
         for (int q = 0; q < CP; ++q) {
-          if (ch >= LAG) {
+          if constexpr (PH == 0) {
+            const int pp = ch * CP + q;
+            wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rn, vn + pp * wrow, 0, CPOL_MASTER_LD));
+          } else if (ch >= LAG) {
             const int pp = (ch - LAG) * CP + q;
             wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rn, vn + pp * wrow, 0, CPOL_MASTER_LD));
-          } else {
+          } else if constexpr (PH == 2) {
             const int pp = (ch - LAG + CHUNKS) * CP + q;
             wold[pp] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, vp + pp * wrow, 0, CPOL_MASTER_LD));
           }
@@ -419,7 +430,10 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
         lds_barrier();  // staging full
       }
       pm0 = m0;
-    }
+    };
+    iteration(std::integral_constant<int, 0>{}, 0);
+    if (nmy >= 1) iteration(std::integral_constant<int, 1>{}, 1);
+    for (int it = 2; it <= nmy; ++it) iteration(std::integral_constant<int, 2>{}, it);
   }
 }
 
