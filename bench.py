@@ -77,10 +77,29 @@ def dw_sgd_bytes(d_out: int, d_in: int, batch: int, act_bytes: int = 2) -> int:
     return d_out * d_in * (4 + 4 + copy) + batch * (d_in + d_out) * act_bytes
 
 
-def cpu_baseline(cfg, sample_batch: int = 0, min_seconds: float = 10.0):
+def cpu_model() -> str:
+    """The host CPU's model name (as lscpu prints it), or "unknown"."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, sample_batch: int = 0, min_seconds: float = 10.0, single_thread_batch: int = 16,
+                 relu_decisions=None):
     """The oracle, as it is, on SGD iterations of the same network over `sample_batch`
     samples (0: the whole batch; the full weights and update are processed either way),
-    repeated until `min_seconds` have passed; the rate is over all iterations."""
+    repeated until `min_seconds` have passed; the rate is over all iterations. Then one
+    iteration on one thread over `single_thread_batch` samples (0: skip).
+
+    Returns (record, first iteration's result): the latter is the oracle's own step from the
+    seeded state over the whole batch (None when the sample is smaller), against which the
+    device's first step is compared. relu_decisions (whole batch only): the device's ReLU
+    derivative decisions of that step, taken by the oracle's backward pass (see
+    oracle.train_step)."""
     import numpy as np
 
     import oracle
@@ -88,23 +107,69 @@ def cpu_baseline(cfg, sample_batch: int = 0, min_seconds: float = 10.0):
     n = sample_batch or cfg.batch
     d = make_mlp_inputs(cfg, seed=0, batch=n)
     bf16 = cfg.dtype == "bf16"
+    mode = "bf16" if bf16 else "f32"
     xv = (bf16_bits_to_f32(d["x_bits"]) if bf16 else d["x"]).astype(np.float64)
-    iters = 0
+    iters, first = 0, None
+    threads = oracle.threads()
     t0 = time.perf_counter()
+    dec = relu_decisions if n == cfg.batch else None
     while True:
-        oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, "bf16" if bf16 else "f32")
+        r = oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, mode, relu_decisions=dec)
+        if iters == 0 and n == cfg.batch:
+            first = {"loss": r["loss"], "w": r["w"], "b": r["b"], "acts": r["acts"]}
+        del r
         iters += 1
         dt = time.perf_counter() - t0
         if dt >= min_seconds:
             break
     flops = iters * cfg.gemm_flops(batch=n)
     whole = "all" if n == cfg.batch else f"{n} of the"
-    return {"value": round(flops / dt / 1e12, 9), "unit": "TFLOP/s", "cores": oracle.threads(),
-            "kind": "oracle",
-            "sample": f"{iters} SGD iteration(s) of the {'-'.join(map(str, cfg.dims))} stack on {whole} "
-                      f"{cfg.batch} samples (full weights and update), "
-                      f"{'bf16-mirrored' if bf16 else 'fp32-mirrored'} fp64 oracle, "
-                      f"{dt:.2f} s = {iters * n / dt:.3f} samples/s"}
+    rec = {"value": round(flops / dt / 1e12, 9), "unit": "TFLOP/s", "cores": threads,
+           "kind": "oracle", "cpu_model": cpu_model(),
+           "sample": f"{iters} SGD iteration(s) of the {'-'.join(map(str, cfg.dims))} stack on {whole} "
+                     f"{cfg.batch} samples (full weights and update), "
+                     f"{'bf16-mirrored' if bf16 else 'fp32-mirrored'} fp64 oracle, "
+                     f"{dt:.2f} s = {iters * n / dt:.3f} samples/s"}
+    if single_thread_batch:
+        m1 = min(single_thread_batch, cfg.batch)
+        sl = slice(0, m1)
+        oracle.set_threads(1)
+        try:
+            t1 = time.perf_counter()
+            oracle.train_step(d["w"], d["b"], xv[sl], d["labels"][sl], cfg.lr, mode)
+            dt1 = time.perf_counter() - t1
+        finally:
+            oracle.set_threads(threads)
+        rec["single_thread"] = {
+            "value": round(cfg.gemm_flops(batch=m1) / dt1 / 1e12, 9), "unit": "TFLOP/s", "cores": 1,
+            "sample": f"1 SGD iteration on {m1} of the {cfg.batch} samples (full weights and update), "
+                      f"{dt1:.2f} s = {m1 / dt1:.3f} samples/s"}
+    return rec, first
+
+
+def parity_vs_oracle(first_dev, w0, b0, ref):
+    """Normwise errors max|g - o| / max|o| of the device's first step against the oracle's
+    first iteration from the same seeded state: the hidden activations, the update W' - W
+    and b' - b of every layer and the loss; and how many ReLU derivative decisions the two
+    sides took differently (the oracle's backward pass takes the device's)."""
+    import numpy as np
+    errs = {"loss": abs(first_dev["loss"] - ref["loss"]) / abs(ref["loss"])}
+    flips = {}
+    for i, xd in enumerate(first_dev["acts"], start=1):
+        xr = ref["acts"][i]
+        errs[f"X{i + 1}"] = float(np.max(np.abs(xd - xr)) / np.max(np.abs(xr)))
+        flips[f"X{i + 1}"] = int(((xd > 0) != (xr > 0)).sum())
+    for i, (wn, bn) in enumerate(zip(first_dev["w"], first_dev["b"])):
+        for tag, new, old, o in (("dW", wn, w0[i], ref["w"][i]), ("db", bn, b0[i], ref["b"][i])):
+            g = new.astype(np.float64) - old
+            r = o - old
+            den = np.max(np.abs(r))
+            errs[f"{tag}{i + 1}"] = float(np.max(np.abs(g - r)) / den) if den > 0 else float(np.max(np.abs(g)))
+    return {"max_normwise_err": max(errs.values()), "per_tensor": {k: float(f"{v:.3e}") for k, v in errs.items()},
+            "relu_decisions_differing": flips,
+            "compared": "first fused step from the seeded state: hidden activations, W' - W and b' - b of every "
+                        "layer, loss (ReLU derivative decisions shared)",
+            "oracle_mode": "bf16-mirrored fp64"}
 
 
 def conv_cpu_baseline(cfg, images: int = 8):
@@ -479,7 +544,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=5)  # the first warm-up step is kept for the parity check
     ap.add_argument("--workload", default="alexnet_fc_b256")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-batch", type=int, default=0, help="samples in the oracle's timed step (0: the whole batch)")
@@ -538,7 +603,16 @@ def main():
     def step():
         m.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss, stream=stream)
 
-    for _ in range(args.warmup):
+    # the first warm-up step starts from the seeded state: kept for the comparison with the oracle
+    first_dev = None
+    if args.warmup >= 1:
+        step()
+        torch.cuda.synchronize()
+        first_dev = {"loss": loss.item(), "w": [l["w"].cpu().numpy() for l in layers],
+                     "b": [l["b"].cpu().numpy() for l in layers],
+                     "acts": [m.ws_view(net, ws, m.IMBD_WS_ACT, i).float().cpu().numpy().astype(np.float64)
+                              for i in range(1, cfg.n_layers)]}
+    for _ in range(max(args.warmup - 1, 0)):
         step()
     torch.cuda.synchronize()
     loss0 = loss.item()
@@ -604,7 +678,14 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(cfg, args.cpu_sample_batch)
+        dec = None if first_dev is None else [None] + first_dev["acts"]
+        result["cpu_baseline"], ref = cpu_baseline(cfg, args.cpu_sample_batch, relu_decisions=dec)
+        if ref is not None and first_dev is not None:
+            w0 = [np.asarray(w, np.float64) for w in d["w"]]
+            b0 = [np.asarray(b, np.float64) for b in d["b"]]
+            result["parity"] = parity_vs_oracle(first_dev, w0, b0, ref)
+            log(f"bench: first step against the oracle, max normwise error "
+                f"{result['parity']['max_normwise_err']:.2e}")
     print(json.dumps(result), flush=True)
 
 

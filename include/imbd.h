@@ -27,7 +27,8 @@
  *   argument returns IMBD_EINVAL and enqueues nothing. A launch failure returns IMBD_EHIP.
  *   imbd_last_error() gives a thread-local description of the last failure. No C++
  *   exception crosses this boundary. Labels outside [0, C) are not read out of bounds;
- *   their sample's loss becomes NaN.
+ *   their sample's loss and its whole row of the top-layer gradient become NaN, so the
+ *   batch loss and every update computed from that gradient are NaN too.
  * - Determinism. Fixed reduction orders: identical inputs give identical bits.
  * - Concurrency. Calls that share a workspace must be ordered on one stream.
  */
@@ -51,8 +52,10 @@ enum imbd_status {
 
 enum imbd_dtype { IMBD_F32 = 0, IMBD_BF16 = 1 };
 
-/* Static description of a string; never NULL. */
+/* Static description of a status code; never NULL. mlp_status_string is the same
+ * function under the name the rest of the mlp_* calls use. */
 const char *imbd_status_string(int status);
+const char *mlp_status_string(int status);
 /* Detail of the last failure on the calling thread ("" if none). */
 const char *imbd_last_error(void);
 /* Library version, major*10000 + minor*100 + patch. */
@@ -213,6 +216,47 @@ int conv3x3_tile_dgrad(int N, int H, int W, int C_in, int C_out, const void *dy_
 int conv3x3_tile_wgrad(int N, int H, int W, int C_in, int C_out, const void *x_pad,
                        const void *dy_pad, float *dw, void *ws, size_t ws_bytes, void *stream);
 size_t conv3x3_wgrad_workspace_bytes(int N, int H, int W, int C_in, int C_out);
+
+/* The tile's whole backward pass (Sec. 2.2; Eq. (7) for what it exchanges): the input
+ * gradient (as conv3x3_tile_dgrad, skipped when dx is NULL) and the partial weight
+ * gradient (as conv3x3_tile_wgrad), on `stream` in that order. Both passes are validated
+ * before either is enqueued; ws must hold conv3x3_wgrad_workspace_bytes. */
+int conv3x3_tile_bwd(int N, int H, int W, int C_in, int C_out, const void *x_pad, const void *w,
+                     const void *dy_pad, void *dx, int dx_dtype, float *dw, void *ws,
+                     size_t ws_bytes, void *stream);
+
+/* ====================================================================================
+ * Options: kernel routing and K splits (for A/B timing and for tests that force a
+ * route; the defaults are the measured choices)
+ * ==================================================================================== */
+enum imbd_option {
+    IMBD_OPT_SKINNY_OFF = 0,    /* 1: forward / Delta_X products of B <= 256 on the tiled template */
+    IMBD_OPT_SKINNY_SPLITS = 1, /* K split of the B <= 256 product kernel, 0 = planned (0..64) */
+    IMBD_OPT_TOP_UNFUSED = 2,   /* 1: the top layer's softmax in a launch of its own */
+    IMBD_OPT_WIDE_OFF = 3,      /* 1: forward / Delta_X products of B > 256 on the tiled template */
+    IMBD_OPT_WIDE_SPLITS = 4,   /* K split of the B > 256 product kernel, 0 = planned */
+    IMBD_OPT_DW_WIDE_MIN_K = 5, /* smallest batch whose fused update runs on the large-tile
+                                   kernel (default 385) */
+    IMBD_OPT_DW_STREAM = 6,     /* 0: past 256 samples the persistent update kernel reloads its
+                                   Delta_Y block per 256 samples instead of streaming it */
+    IMBD_OPT_DW_GENERIC = 7,    /* 1: the fused update on the tiled template */
+    IMBD_OPT_GEMM_CFG = 8,      /* tile configuration of the tiled template, -1 = planned (-1..3) */
+    IMBD_OPT_GEMM_SPLITS = 9,   /* K split of the tiled template, 0 = planned */
+    IMBD_OPT_CONV_NT = 10,      /* 0: the conv tile on the tiled template */
+    IMBD_OPT_COUNT = 11
+};
+/* Each option starts at the value of the environment variable named by
+ * imbd_option_name(key) when the library is loaded (its default if unset or out of
+ * range); the environment is not read again. imbd_set_option changes it for the whole
+ * process: calls made afterwards use the new value. Options that move work between
+ * kernels or change a K split change the workspace the *_workspace_bytes functions
+ * report, so set them before sizing a workspace, and do not change them while another
+ * thread has a call in flight. Returns IMBD_EINVAL for an unknown key or a value outside
+ * the option's range. */
+int imbd_set_option(int key, int value);
+int imbd_get_option(int key, int *value);
+/* The option's environment variable ("IMBD_..."), or "" for an unknown key. */
+const char *imbd_option_name(int key);
 
 /* ====================================================================================
  * Kernel timing (diagnostics for the roofline report)

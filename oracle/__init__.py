@@ -46,18 +46,27 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
-_SO = os.path.join(_HERE, "liboracle.so")
+# ORACLE_LIB names another build of oracle.c to load (the sanitizer build of the tests)
+_SO = os.environ.get("ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
+
+# AddressSanitizer + UndefinedBehaviorSanitizer, every finding fatal (host code only).
+SANITIZE_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=all"]
 
 _MODES = {"f64": 0, "bf16": 1, "f32": 2}
 
 
-def build() -> str:
-    """Compile the oracle with gcc (host only, no device code)."""
-    cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-Wall", _SRC, "-o", _SO + ".tmp", "-lm"]
+def build(out: str | None = None, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (host only, no device code). sanitize: the
+    AddressSanitizer / UndefinedBehaviorSanitizer build (load it with ORACLE_LIB and the
+    sanitizer runtime preloaded)."""
+    out = out or _SO
+    opt = SANITIZE_FLAGS if sanitize else ["-O2"]
+    cmd = ["gcc", *opt, "-fopenmp", "-shared", "-fPIC", "-Wall", _SRC, "-o", out + ".tmp", "-lm"]
     subprocess.check_call(cmd)
-    os.replace(_SO + ".tmp", _SO)
-    return _SO
+    os.replace(out + ".tmp", out)
+    return out
 
 
 def _load():
@@ -70,6 +79,7 @@ def _load():
     d, i, l, p = ctypes.c_double, ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
     sig = {
         "orc_threads": (i, []),
+        "orc_set_threads": (None, [i]),
         "orc_round_bf16": (d, [d]),
         "orc_round_f32": (d, [d]),
         "orc_round_array": (None, [p, l, i]),
@@ -105,6 +115,11 @@ def _ptr(a: np.ndarray):
 
 def threads() -> int:
     return _load().orc_threads()
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads of the loops that follow (the results do not depend on it)."""
+    _load().orc_set_threads(int(n))
 
 
 # ----------------------------------------------------------------------------- rounding
@@ -218,13 +233,21 @@ def forward(ws, bs, x, labels, mode: str = "f64"):
     return {"w_op": wop, "acts": xs, "logits": logits, "loss": loss, "dZ": dZ, "row_loss": rows}
 
 
-def train_step(ws, bs, x, labels, eta: float, mode: str = "f64", want_dx1: bool = False):
+def train_step(ws, bs, x, labels, eta: float, mode: str = "f64", want_dx1: bool = False,
+               relu_decisions=None):
     """One SGD iteration, Sec. 1 and Eq. (1), in the order the paper gives it.
 
     ws, bs: lists of fp32 master weights [d_i][d_{i-1}] and biases [d_i]. x: [B][d_0]
     input values (for "bf16" the bf16 values themselves). Returns a dict with
     activations, loss, every Delta_Y, dW, db, the updated masters/biases and, for
     "bf16", the updated bf16 weight copies (as values).
+
+    relu_decisions: optional list indexed like the activations; entry i (i >= 1), when
+    not None, is a [B][d_i] array whose positive entries mark where f'(Y_{i-1}) = 1, used
+    in place of this iteration's own [X_i > 0]. The derivative of ReLU is a 0/1 decision
+    taken on the sign of a sum; a caller comparing two implementations whose sums differ
+    by rounding passes one side's decisions so that both sides take the same one. Nothing
+    else of the iteration changes.
     """
     L = len(ws)
     st = forward(ws, bs, x, labels, mode)
@@ -239,7 +262,8 @@ def train_step(ws, bs, x, labels, eta: float, mode: str = "f64", want_dx1: bool 
         dWs[i], dbs[i] = dW, db
         if i >= 1:
             dX = input_grad(st["w_op"][i], dY[i])
-            dY[i - 1] = store(relu_mask(dX, st["acts"][i]))
+            dec = None if relu_decisions is None else relu_decisions[i]
+            dY[i - 1] = store(relu_mask(dX, st["acts"][i] if dec is None else dec))
         elif want_dx1:
             dx1 = store(input_grad(st["w_op"][0], dY[0]))
     new_w = [store32(sgd(ws[i], dWs[i], eta)) for i in range(L)]

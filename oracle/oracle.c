@@ -27,6 +27,8 @@
 typedef int64_t i64;
 
 int orc_threads(void) { return omp_get_max_threads(); }
+/* Threads of the parallel loops that follow (n >= 1); the results do not depend on it. */
+void orc_set_threads(int n) { if (n >= 1) omp_set_num_threads(n); }
 
 /* ---------------------------------------------------------------------------------
  * Rounding to the storage formats of the device path.
@@ -60,6 +62,7 @@ double orc_round_f32(double x) { return (double)(float)x; }
 void orc_round_array(double *a, i64 n, int mode)
 {
     if (mode == 0) return;
+#pragma omp parallel for schedule(static)
     for (i64 i = 0; i < n; ++i)
         a[i] = (mode == 1) ? orc_round_bf16(a[i]) : orc_round_f32(a[i]);
 }
@@ -185,6 +188,7 @@ void orc_relu_mask(int din, int B, double *dX, i64 lddx, const double *Xf, i64 l
 /* Mini-batch SGD, Eq. (1): w <- w - eta * g, where g is the mini-batch mean gradient. */
 void orc_sgd(double *w, const double *g, i64 n, double eta)
 {
+#pragma omp parallel for schedule(static)
     for (i64 i = 0; i < n; ++i) w[i] = w[i] - eta * g[i];
 }
 
@@ -225,20 +229,24 @@ void orc_conv3x3_dgrad(int N, int H, int W, int Ci, int Co,
                        const double *dyp, const double *wt, double *dx)
 {
     const i64 Wp = W + 2, Hp = H + 2;
+    /* All Ci outputs of one pixel are accumulated side by side (c innermost, so the
+     * weight rows are read contiguously); each output still sums over r, then q, then o
+     * in ascending order. */
 #pragma omp parallel for collapse(2) schedule(static)
     for (int n = 0; n < N; ++n)
         for (int h = 0; h < H; ++h)
-            for (int w = 0; w < W; ++w)
-                for (int c = 0; c < Ci; ++c) {
-                    double s = 0.0;
-                    for (int r = 0; r < 3; ++r)
-                        for (int q = 0; q < 3; ++q) {
-                            const double *g = dyp + (((i64)n * Hp + h + 2 - r) * Wp + w + 2 - q) * Co;
-                            for (int o = 0; o < Co; ++o)
-                                s += wt[(((i64)o * 3 + r) * 3 + q) * Ci + c] * g[o];
+            for (int w = 0; w < W; ++w) {
+                double *s = dx + (((i64)n * H + h) * W + w) * Ci;
+                for (int c = 0; c < Ci; ++c) s[c] = 0.0;
+                for (int r = 0; r < 3; ++r)
+                    for (int q = 0; q < 3; ++q) {
+                        const double *g = dyp + (((i64)n * Hp + h + 2 - r) * Wp + w + 2 - q) * Co;
+                        for (int o = 0; o < Co; ++o) {
+                            const double *wv = wt + (((i64)o * 3 + r) * 3 + q) * Ci;
+                            for (int c = 0; c < Ci; ++c) s[c] += wv[c] * g[o];
                         }
-                    dx[(((i64)n * H + h) * W + w) * Ci + c] = s;
-                }
+                    }
+            }
 }
 
 /* Weight gradient of the tile: the tile's share of the sum over all pixels that the

@@ -19,13 +19,17 @@ from ._abi import (IMBD_BF16, IMBD_F32, IMBD_K_BIAS, IMBD_K_CAST, IMBD_K_CONV_DG
                    IMBD_EINVAL, IMBD_EUNSUPPORTED, IMBD_EHIP, IMBD_EWORKSPACE,
                    IMBD_WS_ACT, IMBD_WS_DY, IMBD_WS_LOGITS, IMBD_WS_ROWLOSS, ImbdError, Layer,
                    MlpDesc, check, load)
+from ._abi import (IMBD_OPT_CONV_NT, IMBD_OPT_COUNT, IMBD_OPT_DW_GENERIC, IMBD_OPT_DW_STREAM,  # noqa: F401
+                   IMBD_OPT_DW_WIDE_MIN_K, IMBD_OPT_GEMM_CFG, IMBD_OPT_GEMM_SPLITS, IMBD_OPT_SKINNY_OFF,
+                   IMBD_OPT_SKINNY_SPLITS, IMBD_OPT_TOP_UNFUSED, IMBD_OPT_WIDE_OFF, IMBD_OPT_WIDE_SPLITS)
 
 __all__ = [
     "load", "ImbdError", "MLP", "mlp_workspace_bytes", "mlp_workspace_offset", "mlp_fwd",
     "mlp_bwd", "mlp_train_step", "sgd_step", "cast_f32_bf16", "softmax_xent", "mlp_local_fwd",
     "mlp_local_bwd", "mlp_local_workspace_bytes", "conv3x3_tile_fwd", "conv3x3_tile_dgrad",
-    "conv3x3_tile_wgrad", "conv3x3_wgrad_workspace_bytes", "timing_begin", "timing_end",
-    "ws_view", "dtype_code",
+    "conv3x3_tile_wgrad", "conv3x3_tile_bwd", "conv3x3_wgrad_workspace_bytes", "timing_begin",
+    "timing_end",
+    "ws_view", "dtype_code", "set_option", "get_option", "option_name", "options",
 ]
 
 
@@ -222,6 +226,16 @@ def conv3x3_tile_wgrad(x_pad, dy_pad, dw, ws=None, stream=None):
                                  _stream(stream)), "conv3x3_tile_wgrad")
 
 
+def conv3x3_tile_bwd(x_pad, w, dy_pad, dw, dx=None, ws=None, stream=None):
+    """Input gradient (skipped when dx is None) and partial weight gradient of the tile."""
+    lib = load()
+    N, Hp, Wp, Ci = x_pad.shape
+    check(lib.conv3x3_tile_bwd(N, Hp - 2, Wp - 2, Ci, dy_pad.shape[3], _ptr(x_pad), _ptr(w), _ptr(dy_pad),
+                               _ptr(dx), dtype_code(dx) if dx is not None else IMBD_BF16, _ptr(dw), _ptr(ws),
+                               0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)),
+          "conv3x3_tile_bwd")
+
+
 def timing_begin(kernel_class: int, layer: int = -1, max_launches: int = 1000):
     check(load().imbd_timing_begin(kernel_class, layer, max_launches), "imbd_timing_begin")
 
@@ -231,3 +245,37 @@ def timing_end():
     ms = ctypes.c_double(0.0)
     check(load().imbd_timing_end(ctypes.byref(n), ctypes.byref(ms)), "imbd_timing_end")
     return n.value, ms.value
+
+
+def set_option(key: int, value: int):
+    check(load().imbd_set_option(int(key), int(value)), "imbd_set_option")
+
+
+def get_option(key: int) -> int:
+    v = ctypes.c_int(0)
+    check(load().imbd_get_option(int(key), ctypes.byref(v)), "imbd_get_option")
+    return v.value
+
+
+def option_name(key: int) -> str:
+    return load().imbd_option_name(int(key)).decode()
+
+
+class options:
+    """Context manager: set options (key -> value) for a block, restore them after."""
+
+    def __init__(self, **kv):
+        import sys
+        mod = sys.modules[__name__]
+        self.kv = {getattr(mod, "IMBD_OPT_" + k.upper()): int(v) for k, v in kv.items() if v is not None}
+        self.old = {}
+
+    def __enter__(self):
+        for k, v in self.kv.items():
+            self.old[k] = get_option(k)
+            set_option(k, v)
+        return self
+
+    def __exit__(self, *exc):
+        for k, v in self.old.items():
+            set_option(k, v)

@@ -10,6 +10,10 @@ LIB_PATH = os.path.join(HERE, "libimbd.so")
 IMBD_OK, IMBD_EINVAL, IMBD_EUNSUPPORTED, IMBD_EHIP, IMBD_EWORKSPACE = 0, -1, -2, -3, -4
 IMBD_F32, IMBD_BF16 = 0, 1
 IMBD_WS_ACT, IMBD_WS_LOGITS, IMBD_WS_DY, IMBD_WS_ROWLOSS = 0, 1, 2, 3
+(IMBD_OPT_SKINNY_OFF, IMBD_OPT_SKINNY_SPLITS, IMBD_OPT_TOP_UNFUSED, IMBD_OPT_WIDE_OFF, IMBD_OPT_WIDE_SPLITS,
+ IMBD_OPT_DW_WIDE_MIN_K, IMBD_OPT_DW_STREAM, IMBD_OPT_DW_GENERIC, IMBD_OPT_GEMM_CFG, IMBD_OPT_GEMM_SPLITS,
+ IMBD_OPT_CONV_NT) = range(11)
+IMBD_OPT_COUNT = 11
 (IMBD_K_GEMM_FWD, IMBD_K_GEMM_DX, IMBD_K_GEMM_DW, IMBD_K_SPLITK, IMBD_K_SOFTMAX, IMBD_K_BIAS,
  IMBD_K_SGD, IMBD_K_CAST, IMBD_K_CONV_FWD, IMBD_K_CONV_DGRAD, IMBD_K_CONV_WGRAD) = range(11)
 
@@ -31,6 +35,7 @@ _PL = ctypes.POINTER(Layer)
 
 SIGNATURES = {
     "imbd_status_string": (ctypes.c_char_p, [_i]),
+    "mlp_status_string": (ctypes.c_char_p, [_i]),
     "imbd_last_error": (ctypes.c_char_p, []),
     "imbd_version": (_i, []),
     "mlp_workspace_bytes": (_z, [_PD]),
@@ -49,6 +54,10 @@ SIGNATURES = {
     "conv3x3_tile_dgrad": (_i, [_i, _i, _i, _i, _i, _p, _p, _p, _i, _p]),
     "conv3x3_tile_wgrad": (_i, [_i, _i, _i, _i, _i, _p, _p, _p, _p, _z, _p]),
     "conv3x3_wgrad_workspace_bytes": (_z, [_i, _i, _i, _i, _i]),
+    "conv3x3_tile_bwd": (_i, [_i, _i, _i, _i, _i, _p, _p, _p, _p, _i, _p, _p, _z, _p]),
+    "imbd_set_option": (_i, [_i, _i]),
+    "imbd_get_option": (_i, [_i, ctypes.POINTER(ctypes.c_int)]),
+    "imbd_option_name": (ctypes.c_char_p, [_i]),
     "imbd_timing_begin": (_i, [_i, _i, _i]),
     "imbd_timing_end": (_i, [ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)]),
 }

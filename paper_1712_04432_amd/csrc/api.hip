@@ -219,6 +219,8 @@ const char *imbd_status_string(int status) {
   }
 }
 
+const char *mlp_status_string(int status) { return imbd_status_string(status); }
+
 const char *imbd_last_error(void) { return g_err; }
 
 int imbd_version(void) { return 100; }
@@ -584,6 +586,20 @@ int conv3x3_tile_wgrad(int N, int H, int W, int C_in, int C_out, const void *x_p
 size_t conv3x3_wgrad_workspace_bytes(int N, int H, int W, int C_in, int C_out) {
   if (N < 0 || H < 1 || W < 1 || C_in < 1 || C_out < 1) return 0;
   return conv_wgrad_ws_bytes(N, H, W, C_in, C_out);
+}
+
+int conv3x3_tile_bwd(int N, int H, int W, int C_in, int C_out, const void *x_pad, const void *w,
+                     const void *dy_pad, void *dx, int dx_dtype, float *dw, void *ws, size_t ws_bytes,
+                     void *stream) {
+  // validate both passes before enqueueing either
+  TRY(check_conv(N, H, W, C_in, C_out));
+  if (dx && !valid_dtype(dx_dtype)) FAIL(IMBD_EINVAL, "unknown dx dtype");
+  if (!dw) FAIL(IMBD_EINVAL, "dw must be set");
+  if (N > 0 && (!x_pad || !dy_pad || (dx && !w))) FAIL(IMBD_EINVAL, "x_pad, dy_pad (and w with dx) must be set");
+  if (N > 0 && ws_bytes < conv_wgrad_ws_bytes(N, H, W, C_in, C_out))
+    FAIL(IMBD_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, conv_wgrad_ws_bytes(N, H, W, C_in, C_out));
+  if (dx) TRY(conv3x3_tile_dgrad(N, H, W, C_in, C_out, dy_pad, w, dx, dx_dtype, stream));
+  return conv3x3_tile_wgrad(N, H, W, C_in, C_out, x_pad, dy_pad, dw, ws, ws_bytes, stream);
 }
 
 // --------------------------------------------------------------------------- timing

@@ -27,12 +27,14 @@ __device__ __forceinline__ i32x4 buf_rsrc(const void *base, uint32_t bytes) {
 // the buffer; an offset at or past the descriptor's range writes zeros. Issued from
 // inline assembly so that the compiler does not drain the loads at every LDS read: the
 // caller waits for them explicitly (vmcnt) before the barrier that publishes the slab.
-// m0 (the LDS base of the write) is set inside the statement; on gfx9-family parts LDS
-// instructions do not read m0, and nothing else in the kernel that uses it relies on m0.
+// m0 holds the LDS base of the write. It is an operand of the statement ("{m0}"), so the
+// compiler itself writes m0 and knows what it holds: it never keeps a value of its own
+// there across the load. The s_nop covers the wait state between a write of m0 and an
+// LDS-writing load.
 __device__ __forceinline__ void dma16(const i32x4 &rsrc, uint32_t voff, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
                :
-               : "v"(voff), "s"(rsrc), "s"(lds_base)
+               : "v"(voff), "s"(rsrc), "{m0}"(lds_base)
                : "memory");
 }
 

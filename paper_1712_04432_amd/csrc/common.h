@@ -166,6 +166,9 @@ int run_conv_wg(int N, int H, int W, int Ci, int Co, const void *x, const void *
                 int64_t ldp, int64_t sstride, hipStream_t s);
 
 // --------------------------------------------------------------------- host helpers
+// Current value of an option (enum imbd_option), set at load from the environment or by
+// imbd_set_option.
+int opt(int key);
 void set_error(const char *fmt, ...);
 int check_launch(const char *what);
 

@@ -504,8 +504,7 @@ __global__ void __launch_bounds__(512, 1) conv_wg_kernel(CwArgs a) {
 }  // namespace
 
 bool conv_nt_fits(int pass, int N, int H, int W, int Ci, int Co, const void *act, const void *w, const void *out) {
-  const char *env = getenv("IMBD_CONV_NT");  // 0: use the tiled GEMM template instead
-  if (env && atoi(env) == 0) return false;
+  if (opt(IMBD_OPT_CONV_NT) == 0) return false;  // the tiled GEMM template instead
   const int Cn = pass == 1 ? Co : Ci, Ck = pass == 1 ? Ci : Co;
   auto al = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) % 16) == 0; };
   const int64_t rows = (int64_t)N * (H + 2) * (W + 2) + 2 * (W + 2) + 2 + CV_BM;
@@ -515,8 +514,7 @@ bool conv_nt_fits(int pass, int N, int H, int W, int Ci, int Co, const void *act
 }
 
 bool conv_wg_fits(int N, int H, int W, int Ci, int Co, const void *x, const void *dy, const void *dw) {
-  const char *env = getenv("IMBD_CONV_NT");
-  if (env && atoi(env) == 0) return false;
+  if (opt(IMBD_OPT_CONV_NT) == 0) return false;
   auto al = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) % 16) == 0; };
   const int64_t rows = (int64_t)N * (H + 2) * (W + 2) + 2 * (W + 2) + 2 + 64;
   return N >= 1 && H >= 1 && W >= 1 && Co == 256 && Ci >= 128 && Ci % 128 == 0 && al(x) && al(dy) && al(dw) &&

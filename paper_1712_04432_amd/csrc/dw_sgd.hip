@@ -476,10 +476,9 @@ int run_dw_sgd(const GemmProblem &p, hipStream_t s) {
   d.tiles_m = (p.M + 127) / 128;
   d.tiles_n = (p.N + 127) / 128;
   d.spread = (p.epi.ldo * 4) % 8192 == 0;
-  // past 256 samples Delta_Y streams in slabs beside X (IMBD_DW_STREAM=0: the resident
-  // block reloaded per 256-sample chunk instead)
-  const char *env = getenv("IMBD_DW_STREAM");
-  const bool stream = p.K > KMAX_SAMPLES && !(env && atoi(env) == 0);
+  // past 256 samples Delta_Y streams in slabs beside X (option IMBD_OPT_DW_STREAM = 0:
+  // the resident block reloaded per 256-sample chunk instead)
+  const bool stream = p.K > KMAX_SAMPLES && opt(IMBD_OPT_DW_STREAM) != 0;
   // One workgroup per CU at most, and a multiple of the column-block count so that a
   // workgroup's tiles share one Delta_Y column block (kept in LDS).
   const int tiles = d.tiles_m * d.tiles_n;

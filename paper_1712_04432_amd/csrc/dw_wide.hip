@@ -257,8 +257,7 @@ bool dw_wide_fits(const GemmProblem &p) {
   // the fused update: batches above 384 (smaller ones run on the persistent kernel, which
   // streams Delta_Y past 256 samples and is the faster of the two up to 384 on the AlexNet
   // and VGG FC stacks); the fp32 store: any batch
-  const char *env = getenv("IMBD_DW_WIDE_MIN_K");
-  const int min_k = e.mode == EPI_STORE ? 1 : ((env && *env) ? atoi(env) : 385);
+  const int min_k = e.mode == EPI_STORE ? 1 : opt(IMBD_OPT_DW_WIDE_MIN_K);
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const int64_t lim = (int64_t)1 << 31;  // bytes in one buffer descriptor
   if (p.dtype != IMBD_BF16 || p.a_kc || p.b_kc || e.mask || e.bias || e.relu || p.K < min_k || p.K <= 0 ||

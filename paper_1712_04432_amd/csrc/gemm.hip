@@ -829,10 +829,6 @@ const KernelFn kConvFns[2][3] = {
     {gemm_kernel<uint16_t, 128, 128, 2, 2, true, true, 1>, gemm_kernel<uint16_t, 128, 128, 2, 2, false, true, 2>,
      gemm_kernel<uint16_t, 128, 128, 2, 2, false, false, 3>}};
 
-int env_int(const char *name, int dflt) {
-  const char *v = getenv(name);
-  return (v && *v) ? atoi(v) : dflt;
-}
 
 inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
@@ -856,7 +852,7 @@ static GemmPlan tiled_plan(const GemmProblem &p) {
   // A short product whose large tiles cannot fill 256 CUs takes 64 x 64 tiles instead
   // (splitting its few K tiles could not fill them either).
   if (cfg != 0 && ktiles < 16 && cdiv(p.M, kCfgs[cfg].bm) * cdiv(p.N, kCfgs[cfg].bn) < 256) cfg = 0;
-  const int forced = env_int("IMBD_GEMM_CFG", -1);
+  const int forced = opt(IMBD_OPT_GEMM_CFG);
   if (forced >= 0 && forced < kNumCfgs) cfg = forced;
   pl.cfg = cfg;
   pl.bm = kCfgs[cfg].bm;
@@ -872,7 +868,7 @@ static GemmPlan tiled_plan(const GemmProblem &p) {
     if (splits > max_s) splits = max_s;
     if (splits < 1) splits = 1;
   }
-  const int forced_s = env_int("IMBD_GEMM_SPLITS", -1);
+  const int forced_s = opt(IMBD_OPT_GEMM_SPLITS);
   if (forced_s >= 1) splits = forced_s < ktiles ? forced_s : (ktiles > 0 ? ktiles : 1);
   int k_split = cdiv(cdiv(p.K > 0 ? p.K : 1, splits), BK) * BK;
   splits = p.K > 0 ? cdiv(p.K, k_split) : 1;
@@ -890,7 +886,7 @@ GemmPlan gemm_plan(const GemmProblem &p) {
   // any run fits the workspace that the same dimensions were given.
   const GemmPlan tp = tiled_plan(p);
   GemmPlan pl{};
-  if (skinny_dims_fit(p) && env_int("IMBD_SKINNY_OFF", 0) == 0) {
+  if (skinny_dims_fit(p) && opt(IMBD_OPT_SKINNY_OFF) == 0) {
     if (skinny_fits(p)) {
       // the skinny-batch product always goes through fp32 partials (one per K split)
       skinny_plan(p, &pl.splits, &pl.k_split);
@@ -1025,7 +1021,7 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   // fused with the update past 384 samples; the fused update of a smaller batch on the
   // persistent one.
   if (dw_wide_fits(p)) return run_dw_wide(p, s);
-  if (dw_sgd_fits(p) && env_int("IMBD_DW_GENERIC", 0) == 0) return run_dw_sgd(p, s);
+  if (dw_sgd_fits(p) && opt(IMBD_OPT_DW_GENERIC) == 0) return run_dw_sgd(p, s);
   const TileCfg &c = kCfgs[pl.cfg];
   KernelFn fn = c.fn[p.dtype == IMBD_BF16][p.a_kc][p.b_kc];
   const int grid = g.tiles_m * g.tiles_n * g.splits;

@@ -22,7 +22,8 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // One wave per sample row: row maximum, sum of exp(z - max), per-sample loss
-// lse - z[label] and the gradient inv_batch * (softmax - onehot). NPL > 0 keeps the row in
+// lse - z[label] and the gradient inv_batch * (softmax - onehot); a label outside [0, C)
+// gives a NaN loss and a NaN gradient row (no one-hot to subtract). NPL > 0 keeps the row in
 // registers (NPL values per lane, C <= 64*NPL) so the logits are read once; NPL == 0 reads
 // them from memory in each pass (any C).
 template <int NPL>
@@ -65,7 +66,7 @@ __global__ void __launch_bounds__(256)
     for (int j = 0; j < NPL; ++j) {
       const int c = lane + 64 * j;
       if (c < C) {
-        const float g = inv_batch * (v[j] * inv_s - (c == lab ? 1.0f : 0.0f));
+        const float g = ok ? inv_batch * (v[j] * inv_s - (c == lab ? 1.0f : 0.0f)) : __builtin_nanf("");
         if (dz_bf16)
           reinterpret_cast<uint16_t *>(dz)[(int64_t)row * lddz + c] = f32_to_bf16(g);
         else
@@ -74,7 +75,7 @@ __global__ void __launch_bounds__(256)
     }
   } else {
     for (int c = lane; c < C; c += 64) {
-      const float g = inv_batch * (expf(z[c] - mx) * inv_s - (c == lab ? 1.0f : 0.0f));
+      const float g = ok ? inv_batch * (expf(z[c] - mx) * inv_s - (c == lab ? 1.0f : 0.0f)) : __builtin_nanf("");
       if (dz_bf16)
         reinterpret_cast<uint16_t *>(dz)[(int64_t)row * lddz + c] = f32_to_bf16(g);
       else

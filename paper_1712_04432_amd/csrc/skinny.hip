@@ -421,7 +421,7 @@ struct SkSoftmaxArgs {
 // reduce), stored; then softmax cross-entropy over the row: maximum, sum of
 // exp(z - max) (each wave in the shuffle order of the row kernel, the waves' values
 // added in wave order), per-sample loss lse - z[label] and the gradient
-// inv_batch * (softmax - onehot).
+// inv_batch * (softmax - onehot); NaN loss and gradient row for a label outside [0, C).
 __global__ void __launch_bounds__(1024) skinny_softmax_rows(SkSoftmaxArgs g) {
   __shared__ float red[2][16];
   const int row = blockIdx.x, c = threadIdx.x, lane = c & 63, w = c >> 6;
@@ -461,7 +461,8 @@ __global__ void __launch_bounds__(1024) skinny_softmax_rows(SkSoftmaxArgs g) {
   const bool ok = lab >= 0 && lab < g.C;
   if (c == (ok ? lab : 0)) g.row_loss[row] = ok ? (mx + logf(s) - z) : __builtin_nanf("");
   if (in) {
-    const float gr = g.inv_batch * (e * (1.0f / s) - (c == lab ? 1.0f : 0.0f));
+    // a label outside [0, C) has no one-hot: its whole gradient row is NaN, like its loss
+    const float gr = ok ? g.inv_batch * (e * (1.0f / s) - (c == lab ? 1.0f : 0.0f)) : __builtin_nanf("");
     if (g.dz_bf16)
       reinterpret_cast<uint16_t *>(g.dz)[(int64_t)row * g.lddz + c] = f32_to_bf16(gr);
     else
@@ -471,11 +472,6 @@ __global__ void __launch_bounds__(1024) skinny_softmax_rows(SkSoftmaxArgs g) {
 
 int nb_for(int N) { return N <= 64 ? 1 : N <= 128 ? 2 : 4; }
 
-int env_int_skinny(const char *name) {
-  const char *s = getenv(name);
-  return s ? atoi(s) : 0;
-}
-int env_splits() { return env_int_skinny("IMBD_SKINNY_SPLITS"); }
 
 }  // namespace
 
@@ -505,7 +501,7 @@ void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
   const double hbm = 5.0e12, clk = 2.1e9, slab_clk = 900.0, fill_clk = 12000.0;
   int best_s = 1;
   double best_t = 1e30;
-  const int forced = env_splits();
+  const int forced = opt(IMBD_OPT_SKINNY_SPLITS);
   for (int s = 1; s <= 64; ++s) {
     const int ks = ((p.K + s - 1) / s + SK_KS - 1) / SK_KS * SK_KS;
     if ((p.K + ks - 1) / ks != s) continue;
@@ -603,7 +599,7 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
 
 bool skinny_softmax_fits(const GemmProblem &p) {
   return skinny_fits(p) && p.a_kc && p.M <= 1024 && p.epi.relu == 0 && p.epi.mask == nullptr &&
-         p.epi.out_dtype == IMBD_F32 && env_int_skinny("IMBD_TOP_UNFUSED") == 0;
+         p.epi.out_dtype == IMBD_F32 && opt(IMBD_OPT_TOP_UNFUSED) == 0;
 }
 
 int run_skinny_softmax(const GemmProblem &p, void *ws, const int32_t *labels, float inv_batch, float *row_loss,

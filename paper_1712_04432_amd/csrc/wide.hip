@@ -334,8 +334,7 @@ int64_t a_extent(const GemmProblem &p) {
 }  // namespace
 
 bool wide_dims_fit(const GemmProblem &p) {
-  const char *env = getenv("IMBD_WIDE_OFF");  // 1: use the tiled GEMM template instead
-  if (env && atoi(env) != 0) return false;
+  if (opt(IMBD_OPT_WIDE_OFF) != 0) return false;  // the tiled GEMM template instead
   return p.dtype == IMBD_BF16 && p.b_kc && p.db_mode == 0 && p.epi.mode == EPI_STORE && p.M >= 128 &&
          p.N > 256 && p.K >= WD_KS && p.M % 8 == 0 && p.K % 8 == 0;
 }
@@ -360,8 +359,8 @@ void wide_plan(const GemmProblem &p, int *splits, int *kps) {
   int s = (256 + tiles / 2) / tiles;
   if (s > nsl / 8) s = nsl / 8;
   if (s < 1) s = 1;
-  const char *env = getenv("IMBD_WIDE_SPLITS");
-  if (env && atoi(env) >= 1) s = atoi(env) < nsl ? atoi(env) : nsl;
+  const int forced = opt(IMBD_OPT_WIDE_SPLITS);
+  if (forced >= 1) s = forced < nsl ? forced : nsl;
   *kps = (nsl + s - 1) / s;
   *splits = (nsl + *kps - 1) / *kps;
 }

@@ -127,3 +127,73 @@ class _Fake:
 
     def data_ptr(self):
         return self.addr
+
+
+_OPTION_DEFAULTS = {"SKINNY_OFF": 0, "SKINNY_SPLITS": 0, "TOP_UNFUSED": 0, "WIDE_OFF": 0, "WIDE_SPLITS": 0,
+                    "DW_WIDE_MIN_K": 385, "DW_STREAM": 1, "DW_GENERIC": 0, "GEMM_CFG": -1, "GEMM_SPLITS": 0,
+                    "CONV_NT": 1}
+
+
+def _options_in_child(env_extra):
+    """Option values seen by a fresh process whose environment has only env_extra of the
+    IMBD_* variables."""
+    import json
+    import subprocess
+    import sys
+    env = {k: v for k, v in os.environ.items() if not k.startswith("IMBD_")}
+    env.update(env_extra)
+    code = ("import json, paper_1712_04432_amd as m\n"
+            "print(json.dumps({m.option_name(k)[5:]: m.get_option(k) for k in range(m.IMBD_OPT_COUNT)}))")
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
+                         check=True, timeout=120)
+    return json.loads(out.stdout.strip().splitlines()[-1])
+
+
+def test_options_defaults_and_environment_read_once():
+    assert _options_in_child({}) == _OPTION_DEFAULTS
+    got = _options_in_child({"IMBD_DW_WIDE_MIN_K": "500", "IMBD_WIDE_SPLITS": "3", "IMBD_CONV_NT": "7"})
+    assert got["DW_WIDE_MIN_K"] == 500 and got["WIDE_SPLITS"] == 3
+    assert got["CONV_NT"] == 1          # out of range: the default stays
+
+
+def test_options_set_get_and_validation(lib, monkeypatch):
+    import paper_1712_04432_amd as m
+    assert m.option_name(m.IMBD_OPT_DW_WIDE_MIN_K) == "IMBD_DW_WIDE_MIN_K"
+    assert m.option_name(m.IMBD_OPT_COUNT) == ""
+    old = m.get_option(m.IMBD_OPT_WIDE_SPLITS)
+    # the environment is not read after load
+    monkeypatch.setenv("IMBD_WIDE_SPLITS", "5")
+    assert m.get_option(m.IMBD_OPT_WIDE_SPLITS) == old
+    with m.options(wide_splits=3, dw_stream=0):
+        assert m.get_option(m.IMBD_OPT_WIDE_SPLITS) == 3 and m.get_option(m.IMBD_OPT_DW_STREAM) == 0
+    assert m.get_option(m.IMBD_OPT_WIDE_SPLITS) == old and m.get_option(m.IMBD_OPT_DW_STREAM) == 1
+    assert lib.imbd_set_option(m.IMBD_OPT_SKINNY_OFF, 2) == m.IMBD_EINVAL
+    assert lib.imbd_set_option(m.IMBD_OPT_GEMM_CFG, -2) == m.IMBD_EINVAL
+    assert lib.imbd_set_option(m.IMBD_OPT_COUNT, 0) == m.IMBD_EINVAL
+    assert lib.imbd_set_option(-1, 0) == m.IMBD_EINVAL
+    assert lib.imbd_get_option(0, None) == m.IMBD_EINVAL
+    assert m.get_option(m.IMBD_OPT_SKINNY_OFF) == 0
+
+
+def test_workspace_follows_a_split_option(lib):
+    """A forced K split changes the partial sums a product needs; the workspace sized under
+    the option covers it."""
+    import paper_1712_04432_amd as m
+    net = m.MLP((1032, 264, 136), 777, "bf16")
+    base = m.mlp_workspace_bytes(net)
+    with m.options(wide_splits=8):
+        more = m.mlp_workspace_bytes(net)
+    assert more > base and m.mlp_workspace_bytes(net) == base
+
+
+def test_conv_bwd_validates_before_enqueueing(lib):
+    import paper_1712_04432_amd as m
+    p = ctypes.c_void_p(256)
+    # dw missing; bad sizes; unknown dx dtype; workspace too small for the weight gradient
+    assert lib.conv3x3_tile_bwd(2, 56, 56, 256, 256, p, p, p, p, 1, None, p, 1 << 30, None) == m.IMBD_EINVAL
+    assert lib.conv3x3_tile_bwd(2, 0, 56, 256, 256, p, p, p, p, 1, p, p, 1 << 30, None) == m.IMBD_EINVAL
+    assert lib.conv3x3_tile_bwd(2, 56, 56, 256, 256, p, p, p, p, 9, p, p, 1 << 30, None) == m.IMBD_EINVAL
+    need = lib.conv3x3_wgrad_workspace_bytes(32, 56, 56, 256, 256)
+    assert need > 0
+    assert lib.conv3x3_tile_bwd(32, 56, 56, 256, 256, p, p, p, p, 1, p, p, need - 1, None) == m.IMBD_EWORKSPACE
+    assert lib.mlp_status_string(-4) == lib.imbd_status_string(-4)

@@ -2,8 +2,9 @@
 
 bf16 operands with the halo in place; outputs compared normwise: fp32 outputs at 1e-5
 (identical operand bits, only fp32 accumulation differs), bf16 outputs at the 2e-2 bar
-(and one bf16 rounding, 2^-8). Full-size tiles (32 x 56 x 56, 256 -> 256) are checked on
-sampled outputs that the oracle computes one by one."""
+(and one bf16 rounding, 2^-8). The full-size interior tile (32 x 56 x 56, 256 -> 256) is
+checked on every element of all three passes; the corner tile and other full-size shapes
+on sampled outputs that the oracle computes one by one."""
 import numpy as np
 import pytest
 
@@ -86,6 +87,33 @@ def test_conv_tile_full_size_sampled(imbd, dev, border):
     # every output written (no NaN left from the fill) and finite
     import torch
     assert torch.isfinite(y).all().item() and torch.isfinite(dx).all().item() and torch.isfinite(dw).all().item()
+
+
+@pytest.mark.timeout(600)
+def test_conv_tile_full_size_every_element(imbd, dev):
+    """The interior 56x56 tile, batch 32, 256 -> 256 channels: every element of the
+    forward output, of the input gradient and of the tile's partial weight gradient (the
+    tile's share of the all-reduce of Eq. (7)) against the oracle's direct convolution;
+    and conv3x3_tile_bwd (both backward passes in one call) gives the bits of the two
+    separate calls."""
+    import torch
+    _flush("conv full size, every element")
+    N, H, W, C = 32, 56, 56, 256
+    d = make_conv_inputs(N, H, W, C, C, seed=5)
+    xv, wv, dyv = bf16_values(d["x_bits"]), bf16_values(d["w_bits"]), bf16_values(d["dy_bits"])
+    y, dx, dw = _run(imbd, dev, d)
+    ey = nrm_err(host(y), oracle.conv3x3_fwd(xv, wv))
+    ew = nrm_err(host(dw), oracle.conv3x3_wgrad(xv, dyv))
+    ex = nrm_err(host(dx), oracle.conv3x3_dgrad(dyv, wv))
+    _flush(f"conv full size: y {ey:.1e} dx {ex:.1e} dw {ew:.1e}")
+    assert ey < 1e-5 and ex < 1e-5 and ew < 1e-5
+    xd, wd, dyd = dev_bf16_bits(d["x_bits"], dev), dev_bf16_bits(d["w_bits"], dev), dev_bf16_bits(d["dy_bits"], dev)
+    dx2 = torch.full_like(dx, float("nan"))
+    dw2 = torch.full_like(dw, float("nan"))
+    ws = torch.zeros(max(imbd.conv3x3_wgrad_workspace_bytes(N, H, W, C, C), 16), dtype=torch.uint8, device=dev)
+    imbd.conv3x3_tile_bwd(xd, wd, dyd, dw2, dx=dx2, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(dx2, dx) and torch.equal(dw2, dw)
 
 
 def test_conv_tile_128_position_tiles_sampled(imbd, dev):

@@ -1,0 +1,229 @@
+"""Element-by-element parity at the full sizes of the workloads, end to end.
+
+* 9216-4096-4096-1000, B = 256 (the benchmark's step, launched as the benchmark launches
+  it): one fused step against the oracle's iteration from the same seeded inputs, every
+  element of X_2, X_3, the logits, every Delta_Y_i, W' - W and b' - b of every layer,
+  the loss, and the bf16 weight copies bit for bit as the rounding of the new masters.
+  The ReLU derivative decisions are compared (few may differ, each within the forward bar
+  of zero), then shared with the oracle's backward pass. Then ten steps on one batch,
+  each checked in full against the oracle's step from the device's own state, and the
+  free-running loss curve against the oracle's.
+* 25088-4096-4096-1000, B = 512: one fused step, every element as above.
+* One layer at a time, every process of a 4 x 16 grid at global B = 1024 (local
+  B = 64): the local products of all 64 processes, reassembled by software collectives
+  in fp64 (concatenation over P_r, sums over P_c and over P_r), against the oracle's
+  unpartitioned products (Sec. 2.3, Eq. (8); App. A).
+
+Bars: 2e-2 normwise for quantities downstream of a bf16 storage point; 1e-5 where the
+operands are identical bf16 bits and only fp32 accumulation differs.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from synthdata import get_config, make_local_inputs, make_mlp_inputs
+from tests._util import (TOL_BF16, bf16_values, dev_bf16_bits, host, input_on_device, make_layers,
+                         nrm_err, workspace)
+
+pytestmark = pytest.mark.gpu
+
+TOL_EXACT_OPERANDS = 1e-5
+
+
+def _flush(msg):
+    print(msg, flush=True)
+
+
+def _setup(imbd, cfg, dev, seed=0):
+    import torch
+    d = make_mlp_inputs(cfg, seed=seed)
+    net = imbd.MLP(cfg.dims, cfg.batch, cfg.dtype)
+    layers = make_layers(imbd, d, dev, cfg.dtype)
+    x, xv = input_on_device(d, dev, cfg.dtype)
+    lab = torch.from_numpy(d["labels"]).to(dev)
+    ws = workspace(imbd, net, dev)
+    loss = torch.zeros(1, device=dev)
+    return d, net, layers, x, xv, lab, ws, loss
+
+
+def _device_decisions(imbd, net, ws):
+    """The device's ReLU derivative decisions: its stored activations X_2..X_L (positive
+    where f'(Y) = 1), indexed like the oracle's activations."""
+    return [None] + [host(imbd.ws_view(net, ws, imbd.IMBD_WS_ACT, i)) for i in range(1, net.n_layers)]
+
+
+def _check_step_every_element(imbd, net, layers, ws, loss, w0, b0, xv, labels, lr, tag):
+    """Compare one device step (already run from masters w0 / biases b0) with the oracle's
+    iteration from the same state, element by element. Returns the largest normwise error.
+
+    The forward pass, the loss and the top gradient are the oracle's own. The ReLU
+    derivative is a 0/1 decision on the sign of a sum that the two sides round
+    differently, and one entry decided the other way changes that gradient entry by O(1):
+    so the decisions are compared first (the share that differ is bounded, and each
+    differing one lies within the forward bar of zero on both sides), and the oracle's
+    backward pass then takes the device's decisions."""
+    L = net.n_layers
+    dec = _device_decisions(imbd, net, ws)
+    ref = oracle.train_step(w0, b0, xv, labels, lr, "bf16", relu_decisions=dec)
+    errs, flips = {}, {}
+    errs["loss"] = abs(loss.item() - ref["loss"]) / abs(ref["loss"])
+    for i in range(1, L):
+        xd, xr = dec[i], ref["acts"][i]
+        errs[f"X{i + 1}"] = nrm_err(xd, xr)
+        diff = (xd > 0) != (xr > 0)
+        flips[f"X{i + 1}"] = int(diff.sum())
+        bound = TOL_BF16 * np.max(np.abs(xr))
+        assert np.all(np.abs(xr[diff]) <= bound) and np.all(np.abs(xd[diff]) <= bound), (tag, i)
+        assert diff.mean() < 1e-3, (tag, i, diff.mean())
+    errs["logits"] = nrm_err(host(imbd.ws_view(net, ws, imbd.IMBD_WS_LOGITS)), ref["logits"])
+    for i in range(1, L + 1):
+        errs[f"dY{i}"] = nrm_err(host(imbd.ws_view(net, ws, imbd.IMBD_WS_DY, i)), ref["dY"][i - 1])
+    for i in range(L):
+        wn = host(layers[i]["w"])
+        errs[f"dW{i + 1}"] = nrm_err(wn - w0[i], ref["w"][i] - w0[i])
+        errs[f"db{i + 1}"] = nrm_err(host(layers[i]["b"]) - b0[i], ref["b"][i] - b0[i])
+        assert np.array_equal(host(layers[i]["w_lp"]), oracle.round_bf16(wn)), f"{tag}: bf16 copy of layer {i + 1}"
+    del ref
+    worst = max(errs.values())
+    _flush(f"{tag}: worst normwise error {worst:.2e}; decisions differing {flips}; "
+           + " ".join(f"{k}={v:.1e}" for k, v in errs.items()))
+    for k, v in errs.items():
+        assert v < TOL_BF16, (tag, k, v)
+    return worst
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name", ["alexnet_fc_b256", "vgg_fc_b512"])
+def test_full_size_one_step_every_element(imbd, dev, name):
+    import torch
+    cfg = get_config(name)
+    _flush(f"full-size step {name}: dims {cfg.dims} B={cfg.batch}")
+    d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev)
+    w0 = [host(l["w"]) for l in layers]
+    b0 = [host(l["b"]) for l in layers]
+    imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
+    torch.cuda.synchronize()
+    _check_step_every_element(imbd, net, layers, ws, loss, w0, b0, xv, d["labels"], cfg.lr, name)
+
+
+@pytest.mark.timeout(900)
+def test_alexnet_fc_b256_ten_steps_every_element(imbd, dev):
+    """Ten fused steps of the benchmark's workload on one fixed batch. Each step is checked
+    in full against the oracle's step from the device's own state (masters and biases read
+    back), so each of the ten updates is held to the bar without the trajectory noise of
+    two bf16 implementations; the free-running loss curves must agree and fall."""
+    import torch
+    cfg = get_config("alexnet_fc_b256")
+    _flush("full-size ten steps alexnet_fc_b256")
+    d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev)
+    ws_o, bs_o = [w.astype(np.float64) for w in d["w"]], [b.astype(np.float64) for b in d["b"]]
+    losses_g, losses_o, worst = [], [], 0.0
+    for t in range(cfg.steps):
+        w_dev = [host(l["w"]) for l in layers]
+        b_dev = [host(l["b"]) for l in layers]
+        imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
+        torch.cuda.synchronize()
+        losses_g.append(loss.item())
+        worst = max(worst, _check_step_every_element(imbd, net, layers, ws, loss, w_dev, b_dev, xv,
+                                                     d["labels"], cfg.lr, f"step {t}"))
+        free = oracle.train_step(ws_o, bs_o, xv, d["labels"], cfg.lr, "bf16")
+        losses_o.append(free["loss"])
+        ws_o, bs_o = free["w"], free["b"]
+        del free
+    _flush(f"ten steps: worst {worst:.2e}; losses device {losses_g} oracle {losses_o}")
+    assert losses_o[-1] < losses_o[0] and losses_g[-1] < losses_g[0]
+    assert nrm_err(losses_g, losses_o) < TOL_BF16
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("layer", [1, 2, 3])
+def test_alexnet_local_4x16_whole_grid(imbd, dev, layer):
+    """Every process (r, c) of the 4 x 16 grid runs mlp_local_fwd / mlp_local_bwd on its
+    blocks of one layer of the 9216-4096-4096-1000 stack at global B = 1024, reading its
+    blocks as views of the global tensors (W_i row block, X_i sample block, Delta_Y_i
+    sample x row block) and writing Y straight into its block of the global output.
+    Collectives in software: Y is its blocks side by side, the Delta_W / db partials are
+    summed over the 16 processes of a grid row, the masked Delta_X partials over the 4 of
+    a grid column. Layer 1 has no Delta_X (the backward sum starts at layer 2)."""
+    import torch
+    cfg = get_config("alexnet_fc_local_4x16")
+    P_r, P_c = cfg.grid
+    B = cfg.batch
+    dout, din = cfg.dims[layer], cfg.dims[layer - 1]
+    mb, bb = dout // P_r, B // P_c
+    top = layer == cfg.n_layers
+    _flush(f"4x16 grid, layer {layer}: W {dout}x{din}, B={B}, blocks {mb}x{din} x {bb} samples")
+    g = make_local_inputs(dout, din, B, seed=40 + layer)
+    W, X, DY = bf16_values(g["w_bits"]), bf16_values(g["x_bits"]), bf16_values(g["dy_bits"])
+    bias = g["b"].astype(np.float64)
+    wd, xd, dyd = dev_bf16_bits(g["w_bits"], dev), dev_bf16_bits(g["x_bits"], dev), dev_bf16_bits(g["dy_bits"], dev)
+    bd = torch.from_numpy(g["b"]).to(dev)
+    y = torch.full((B, dout), float("nan"), device=dev, dtype=torch.float32 if top else torch.bfloat16)
+    dW = np.zeros((dout, din))
+    db = np.zeros(dout)
+    dX = np.zeros((B, din))
+    nws = max(imbd.mlp_local_workspace_bytes(w, imbd.IMBD_BF16, mb, din, bb) for w in (0, 1))
+    wsb = torch.zeros(max(nws, 16), dtype=torch.uint8, device=dev)
+    dwp = torch.empty((mb, din), device=dev)
+    dbp = torch.empty(mb, device=dev)
+    dxp = torch.empty((bb, din), device=dev) if layer >= 2 else None
+    for r in range(P_r):
+        rs = oracle.block_rows(dout, P_r, r)
+        for c in range(P_c):
+            cs = oracle.block_rows(B, P_c, c)
+            imbd.mlp_local_fwd(wd[rs], xd[cs], y[cs, rs], P_r, P_c, bias=bd[rs], relu=not top, ws=wsb)
+            imbd.mlp_local_bwd(wd[rs], dyd[cs, rs], xd[cs], dwp, P_r, P_c, db_part=dbp, dx_part=dxp,
+                               mask_relu=layer >= 2, ws=wsb)
+            torch.cuda.synchronize()
+            dW[rs] += host(dwp)          # all-reduce over the P_c processes of grid row r
+            db[rs] += host(dbp)
+            if dxp is not None:
+                dX[cs] += host(dxp)      # all-reduce over the P_r processes of grid column c
+    yref = oracle.affine_fwd(W, X, bias)
+    if top:
+        e = nrm_err(host(y), yref)
+        assert e < TOL_EXACT_OPERANDS, e
+    else:
+        e = nrm_err(host(y), oracle.round_bf16(oracle.relu(yref)))
+        assert e < 2.0 ** -8, e
+    rdw, rdb = oracle.weight_grad(DY, X, 1.0 / B)
+    ew, eb = nrm_err(dW, rdw), nrm_err(db, rdb)
+    ex = 0.0
+    if layer >= 2:
+        ex = nrm_err(dX, oracle.relu_mask(oracle.input_grad(W, DY), X))
+    _flush(f"layer {layer}: Y {e:.1e} dW {ew:.1e} db {eb:.1e} dX {ex:.1e}")
+    assert ew < TOL_EXACT_OPERANDS and eb < TOL_EXACT_OPERANDS and ex < TOL_EXACT_OPERANDS
+
+
+def test_alexnet_fc_b256_resume_is_bit_identical(imbd, dev):
+    """Checkpoint / resume: five steps, the masters, biases and bf16 copies saved to host
+    memory, reloaded into fresh device tensors (and a fresh workspace), five more steps:
+    bit-identical to ten uninterrupted steps. The iteration keeps no state outside the
+    parameters and the batch."""
+    import torch
+    cfg = get_config("alexnet_fc_b256")
+    _flush("resume after five steps")
+    d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev)
+    for _ in range(10):
+        imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
+    torch.cuda.synchronize()
+    straight = [{k: l[k].cpu() for k in ("w", "w_lp", "b")} for l in layers]
+    loss_straight = loss.item()
+    d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev)
+    for _ in range(5):
+        imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
+    torch.cuda.synchronize()
+    saved = [{k: l[k].cpu().numpy().copy() if k != "w_lp" else l[k].view(torch.int16).cpu().numpy().copy()
+              for k in ("w", "w_lp", "b")} for l in layers]
+    del layers, ws
+    torch.cuda.empty_cache()
+    layers = [{"w": torch.from_numpy(s["w"]).to(dev), "b": torch.from_numpy(s["b"]).to(dev),
+               "w_lp": torch.from_numpy(s["w_lp"]).to(dev).view(torch.bfloat16)} for s in saved]
+    ws = workspace(imbd, net, dev)
+    for _ in range(5):
+        imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
+    torch.cuda.synchronize()
+    assert loss.item() == loss_straight
+    for a, b in zip(straight, layers):
+        for k in ("w", "w_lp", "b"):
+            assert torch.equal(a[k], b[k].cpu()), k

@@ -94,16 +94,53 @@ def test_softmax_xent(imbd, dev, B, C, dz_dtype):
         assert nrm_err(host(dz), rdz) < 1e-6
 
 
-def test_softmax_bad_label_gives_nan_not_a_fault(imbd, dev):
+@pytest.mark.parametrize("dz_dtype", ["f32", "bf16"])
+def test_softmax_bad_label_gives_nan_not_a_fault(imbd, dev, dz_dtype):
+    """A label outside [0, C) makes its sample's loss and its whole gradient row NaN (there
+    is no one-hot to subtract), so the corruption cannot reach an update unseen; the other
+    rows are untouched."""
     import torch
     z = dev_f32(np.zeros((4, 10), np.float32), dev)
     lab = torch.tensor([0, 10, -1, 9], dtype=torch.int32, device=dev)
     loss = torch.zeros(1, device=dev)
     rows = torch.zeros(4, device=dev)
-    imbd.softmax_xent(z, lab, 0.25, loss, rows)
+    dz = torch.zeros((4, 10), device=dev, dtype=torch.float32 if dz_dtype == "f32" else torch.bfloat16)
+    imbd.softmax_xent(z, lab, 0.25, loss, rows, dz)
     r = rows.cpu().numpy()
-    assert np.isnan(r[1]) and np.isnan(r[2])
+    g = host(dz)
+    assert np.isnan(r[1]) and np.isnan(r[2]) and np.isnan(loss.item())
     assert r[0] == pytest.approx(np.log(10), rel=1e-6) and r[3] == pytest.approx(np.log(10), rel=1e-6)
+    assert np.isnan(g[1]).all() and np.isnan(g[2]).all()
+    for i in (0, 3):
+        _, ref, _ = oracle.softmax_xent(np.zeros((1, 10)), [int(lab[i])], 0.25)
+        assert np.isfinite(g[i]).all() and nrm_err(g[i], ref[0]) < 1e-2
+
+
+def test_fused_top_layer_bad_label_gives_nan_row(imbd, dev):
+    """The same through the top layer's fused split reduce + softmax (mlp_fwd at a shape
+    whose top product runs on the B <= 256 product kernel)."""
+    import torch
+    from synthdata import make_mlp_inputs, scaled_mlp
+    from tests._util import input_on_device, make_layers, workspace
+    cfg = scaled_mlp((576, 320, 256, 100), 64, "bf16")
+    d = make_mlp_inputs(cfg, seed=2)
+    net = imbd.MLP(cfg.dims, cfg.batch, "bf16")
+    layers = make_layers(imbd, d, dev, "bf16")
+    x, _ = input_on_device(d, dev, "bf16")
+    lab_h = d["labels"].copy()
+    lab_h[5], lab_h[17] = 100, -3
+    lab = torch.from_numpy(lab_h).to(dev)
+    ws = workspace(imbd, net, dev)
+    loss = torch.zeros(1, device=dev)
+    imbd.mlp_fwd(net, layers, x, lab, ws, loss)
+    torch.cuda.synchronize()
+    rl = host(imbd.ws_view(net, ws, imbd.IMBD_WS_ROWLOSS))
+    dy = host(imbd.ws_view(net, ws, imbd.IMBD_WS_DY, 3))
+    bad = np.zeros(64, bool)
+    bad[[5, 17]] = True
+    assert np.isnan(loss.item())
+    assert np.isnan(rl[bad]).all() and np.isfinite(rl[~bad]).all()
+    assert np.isnan(dy[bad]).all() and np.isfinite(dy[~bad]).all()
 
 
 # ------------------------------------------------------------------ local products

@@ -115,22 +115,21 @@ def test_bf16_fused_update_matches_oracle(imbd, dev, dims, B):
     _check_fused_update(imbd, dev, dims, B)
 
 
-# the switches that route the fused update past 256 samples (read at every launch)
-_UPDATE_ROUTES = {"streamed": {"IMBD_DW_WIDE_MIN_K": "100000"},
-                  "reload": {"IMBD_DW_WIDE_MIN_K": "100000", "IMBD_DW_STREAM": "0"},
-                  "wide": {"IMBD_DW_WIDE_MIN_K": "257"}}
+# the options that route the fused update past 256 samples
+_UPDATE_ROUTES = {"streamed": {"dw_wide_min_k": 100000},
+                  "reload": {"dw_wide_min_k": 100000, "dw_stream": 0},
+                  "wide": {"dw_wide_min_k": 257}}
 
 
 @pytest.mark.parametrize("route", sorted(_UPDATE_ROUTES))
 @pytest.mark.parametrize("dims,B", [((264, 128, 24), 300), ((1032, 264, 16), 777), ((2056, 520, 16), 2048)])
-def test_bf16_fused_update_every_kernel_past_256_samples(imbd, dev, monkeypatch, dims, B, route):
+def test_bf16_fused_update_every_kernel_past_256_samples(imbd, dev, dims, B, route):
     """Past 256 samples three kernels can apply the fused update: the persistent one with
     Delta_Y streamed in slabs (the default up to 384 samples), the persistent one with its
     resident Delta_Y block reloaded per 256-sample chunk, and the large-tile one (the
     default past 384). Each is forced in turn, up to the persistent kernel's 2048 samples."""
-    for k, v in _UPDATE_ROUTES[route].items():
-        monkeypatch.setenv(k, v)
-    _check_fused_update(imbd, dev, dims, B)
+    with imbd.options(**_UPDATE_ROUTES[route]):
+        _check_fused_update(imbd, dev, dims, B)
 
 
 def _check_fused_update(imbd, dev, dims, B):

@@ -2,11 +2,8 @@
 kernel at their edges, through the local-block entry points: ragged batch tails (a last
 sample tile of one sample), ragged row tiles, K tails of 8, both operand layouts (W rows
 for the forward, W k-rows for Delta_X), the bias / ReLU / ReLU' mask epilogues, bf16 and
-fp32 outputs, and forced K splits (the split count is read at every launch, so the
-workspace is sized under the same setting). The weight-gradient kernel's fp32 store runs
+fp32 outputs, and forced K splits (the workspace is sized under the same setting). The weight-gradient kernel's fp32 store runs
 at any batch: a single sample, a ragged 65, and output rows fewer than one tile."""
-import os
-
 import numpy as np
 import pytest
 
@@ -20,18 +17,10 @@ TOL_F32_OUT = 1e-5     # fp32 outputs of exact bf16 products, fp32 accumulation
 TOL_BF16_OUT = 2.0 ** -8
 
 
-class _splits:
-    """Force the wide kernel's K split for the duration of a block."""
-
-    def __init__(self, n):
-        self.n = n
-
-    def __enter__(self):
-        if self.n is not None:
-            os.environ["IMBD_WIDE_SPLITS"] = str(self.n)
-
-    def __exit__(self, *exc):
-        os.environ.pop("IMBD_WIDE_SPLITS", None)
+def _splits(n):
+    """Force the wide kernel's K split for the duration of a block (None: planned)."""
+    import paper_1712_04432_amd as m
+    return m.options(wide_splits=n)
 
 
 def _blocks(dout, din, b, seed, dev):

@@ -136,6 +136,73 @@ def test_round_bf16_hand_cases():
     assert np.isnan(r([np.nan])[0])
 
 
+def _nearest_f32_brute_force(x: float) -> float:
+    """The binary32 value nearest to x, ties to the even significand, found by exact
+    rational comparison of the neighbours of x in the binary32 grid (independent of the
+    C conversion the oracle uses)."""
+    from fractions import Fraction
+    if x == 0.0:
+        return x
+    big = np.float32(np.finfo(np.float32).max)
+    if abs(x) > float(big):
+        lo = big
+        hi_val = Fraction(2) ** 128          # where the grid would continue past the maximum
+    else:
+        lo = np.float32(x)                   # a grid point next to x (either side)
+        if Fraction(float(lo)) > Fraction(x):
+            lo = np.nextafter(lo, np.float32(-np.inf))
+        hi = np.nextafter(lo, np.float32(np.inf))
+        hi_val = Fraction(float(hi))
+    fx, flo = Fraction(x), Fraction(float(lo))
+    dlo, dhi = fx - flo, hi_val - fx
+    if dlo < dhi:
+        return float(lo)
+    if dhi < dlo:
+        return float(hi_val) if hi_val < Fraction(2) ** 128 else np.inf
+    even_lo = int(np.array(lo, np.float32).view(np.uint32)) % 2 == 0
+    if even_lo:
+        return float(lo)
+    return float(hi_val) if hi_val < Fraction(2) ** 128 else np.inf
+
+
+def test_round_f32_matches_numpy_cast_and_brute_force():
+    """binary32 storage rounding (masters, biases, gradients and logits of the bf16 and f32
+    modes): against numpy's double -> float cast over the whole binary32 range, and on a
+    subset against the exact nearest grid point."""
+    rng = np.random.default_rng(14)
+    x = np.concatenate([
+        rng.standard_normal(20000) * 10.0 ** rng.integers(-46, 39, 20000),
+        rng.standard_normal(2000) * 2.0 ** -140,                              # subnormal range
+    ])
+    f = rng.standard_normal(4000).astype(np.float32)
+    f = f[np.isfinite(f) & (f != 0)]
+    up = np.nextafter(f, np.float32(np.inf)).astype(np.float64)
+    mid = (f.astype(np.float64) + up) / 2.0                                   # exact ties, both parities
+    x = np.concatenate([x, mid, [0.0, -0.0, 2.0 ** -150, -(2.0 ** -150), 1.5 * 2.0 ** -149]])
+    x = x[np.abs(x) < 3.0e38]
+    got = oracle.round_to(x, "f32")
+    assert np.array_equal(got, x.astype(np.float32).astype(np.float64))
+    for v in np.concatenate([x[::97], mid[:200]]):
+        assert oracle.round_to([v], "f32")[0] == _nearest_f32_brute_force(float(v)), v
+
+
+def test_round_f32_hand_cases():
+    r = lambda v: oracle.round_to([v], "f32")[0]
+    u = 2.0 ** -23                                    # binary32 ulp at 1
+    assert r(1 + u / 2) == 1.0                        # tie, 1 is even
+    assert r(1 + 3 * u / 2) == 1 + 2 * u              # tie, rounds up to even
+    assert r(1 + u / 2 + 2.0 ** -50) == 1 + u         # just above the tie
+    assert r(-(1 + 3 * u / 2)) == -(1 + 2 * u)
+    assert r(2.0 ** -150) == 0.0                      # half the smallest subnormal: tie to 0
+    assert r(1.5 * 2.0 ** -149) == 2.0 ** -148        # subnormal tie, to even
+    assert r(2.0 ** -150 * (1 + 2.0 ** -20)) == 2.0 ** -149
+    fmax = float(np.finfo(np.float32).max)
+    assert r(fmax) == fmax
+    assert r(fmax + 2.0 ** 103) == np.inf             # midpoint to 2^128: tie to even -> inf
+    assert r(fmax + 2.0 ** 102) == fmax
+    assert np.isnan(r(np.nan)) and r(np.inf) == np.inf
+
+
 # ------------------------------------------------------------------- closed forms
 def test_zero_top_layer_gives_log_c_and_uniform_gradient():
     cfg = scaled_mlp((20, 16, 10), 8, "f32", x_dist="uniform01")
@@ -220,6 +287,26 @@ def test_invariants_of_one_step():
     # ReLU mask: entries with zero activation get zero gradient
     for i in (1, 2):
         assert np.all(st["dY"][i - 1][st["acts"][i] == 0] == 0)
+
+
+def test_shared_relu_decisions_replace_only_the_mask():
+    """Passing the iteration's own decisions changes nothing; deciding every unit off
+    zeroes every gradient below the top layer and leaves the forward pass and the top
+    layer's gradient as they were."""
+    cfg = scaled_mlp((20, 12, 8, 5), 6, "bf16")
+    d = make_mlp_inputs(cfg, seed=12)
+    x = bf16_bits_to_f32(d["x_bits"])
+    own = oracle.train_step(d["w"], d["b"], x, d["labels"], 0.01, "bf16")
+    same = oracle.train_step(d["w"], d["b"], x, d["labels"], 0.01, "bf16", relu_decisions=own["acts"])
+    for k in ("dY", "dW", "db", "w", "b"):
+        for a, b in zip(own[k], same[k]):
+            assert np.array_equal(a, b), k
+    off = [None] + [np.zeros_like(a) for a in own["acts"][1:]]
+    z = oracle.train_step(d["w"], d["b"], x, d["labels"], 0.01, "bf16", relu_decisions=off)
+    assert np.array_equal(z["logits"], own["logits"]) and z["loss"] == own["loss"]
+    assert np.array_equal(z["dY"][2], own["dY"][2]) and np.array_equal(z["dW"][2], own["dW"][2])
+    for i in (0, 1):
+        assert not z["dY"][i].any() and not z["dW"][i].any() and not z["db"][i].any()
 
 
 def test_bf16_mode_rounds_exactly_at_storage_points():
