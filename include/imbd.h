@@ -123,6 +123,21 @@ int mlp_train_step(const imbd_mlp_desc *desc, imbd_layer *layers, const void *x,
                    const int32_t *labels, void *ws, size_t ws_bytes, float lr, float *loss,
                    void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): mlp_train_step with its workspace
+ * taken from a scratch array inside the library instead of a ws argument. The array
+ * holds IMBD_STATIC_SCRATCH_BYTES on every GPU the library runs on, from the library's
+ * load until the process ends; the call itself allocates nothing. The caller still
+ * passes parameters, input, labels and the loss. Results are those of mlp_train_step.
+ * Returns IMBD_EWORKSPACE, enqueueing nothing, when mlp_workspace_bytes(desc) exceeds
+ * the scratch (the 9216-4096-4096-1000 stack at B = 256 needs 46 MiB, 25088-4096-4096-1000
+ * at B = 512 needs 53 MiB). All calls on one GPU share that GPU's one array, which keeps
+ * the last call's contents: calls that overlap on one GPU (other streams, other threads)
+ * race, so order them on one stream. The current device must be the stream's device. */
+#define IMBD_STATIC_SCRATCH_BYTES (64u << 20)
+int mlp_train_step_static(const imbd_mlp_desc *desc, imbd_layer *layers, const void *x,
+                          const int32_t *labels, float lr, float *loss, void *stream);
+
 /* ====================================================================================
  * Update and conversion
  * ==================================================================================== */

@@ -19,13 +19,14 @@ from ._abi import (IMBD_BF16, IMBD_F32, IMBD_K_BIAS, IMBD_K_CAST, IMBD_K_CONV_DG
                    IMBD_EINVAL, IMBD_EUNSUPPORTED, IMBD_EHIP, IMBD_EWORKSPACE,
                    IMBD_WS_ACT, IMBD_WS_DY, IMBD_WS_LOGITS, IMBD_WS_ROWLOSS, ImbdError, Layer,
                    MlpDesc, check, load)
+from ._abi import IMBD_STATIC_SCRATCH_BYTES  # noqa: F401
 from ._abi import (IMBD_OPT_CONV_NT, IMBD_OPT_COUNT, IMBD_OPT_DW_GENERIC, IMBD_OPT_DW_STREAM,  # noqa: F401
                    IMBD_OPT_DW_WIDE_MIN_K, IMBD_OPT_GEMM_CFG, IMBD_OPT_GEMM_SPLITS, IMBD_OPT_SKINNY_OFF,
                    IMBD_OPT_SKINNY_SPLITS, IMBD_OPT_TOP_UNFUSED, IMBD_OPT_WIDE_OFF, IMBD_OPT_WIDE_SPLITS)
 
 __all__ = [
     "load", "ImbdError", "MLP", "mlp_workspace_bytes", "mlp_workspace_offset", "mlp_fwd",
-    "mlp_bwd", "mlp_train_step", "sgd_step", "cast_f32_bf16", "softmax_xent", "mlp_local_fwd",
+    "mlp_bwd", "mlp_train_step", "mlp_train_step_static", "sgd_step", "cast_f32_bf16", "softmax_xent", "mlp_local_fwd",
     "mlp_local_bwd", "mlp_local_workspace_bytes", "conv3x3_tile_fwd", "conv3x3_tile_dgrad",
     "conv3x3_tile_wgrad", "conv3x3_tile_bwd", "conv3x3_wgrad_workspace_bytes", "timing_begin",
     "timing_end",
@@ -147,6 +148,14 @@ def mlp_train_step(net: MLP, layers, x, labels, ws, lr: float, loss, stream=None
     arr = _layers(layers)
     check(lib.mlp_train_step(net.desc, arr, _ptr(x), _ptr(labels), _ptr(ws), ws.numel() * ws.element_size(),
                              float(lr), _ptr(loss), _stream(stream)), "mlp_train_step")
+
+
+def mlp_train_step_static(net: MLP, layers, x, labels, lr: float, loss, stream=None):
+    """mlp_train_step on the library's static scratch (no workspace argument, no allocation)."""
+    lib = load()
+    arr = _layers(layers)
+    check(lib.mlp_train_step_static(net.desc, arr, _ptr(x), _ptr(labels), float(lr), _ptr(loss), _stream(stream)),
+          "mlp_train_step_static")
 
 
 def sgd_step(w, grad, lr: float, grad_scale: float = 1.0, w_lp=None, stream=None):

@@ -14,6 +14,7 @@ IMBD_WS_ACT, IMBD_WS_LOGITS, IMBD_WS_DY, IMBD_WS_ROWLOSS = 0, 1, 2, 3
  IMBD_OPT_DW_WIDE_MIN_K, IMBD_OPT_DW_STREAM, IMBD_OPT_DW_GENERIC, IMBD_OPT_GEMM_CFG, IMBD_OPT_GEMM_SPLITS,
  IMBD_OPT_CONV_NT) = range(11)
 IMBD_OPT_COUNT = 11
+IMBD_STATIC_SCRATCH_BYTES = 64 << 20
 (IMBD_K_GEMM_FWD, IMBD_K_GEMM_DX, IMBD_K_GEMM_DW, IMBD_K_SPLITK, IMBD_K_SOFTMAX, IMBD_K_BIAS,
  IMBD_K_SGD, IMBD_K_CAST, IMBD_K_CONV_FWD, IMBD_K_CONV_DGRAD, IMBD_K_CONV_WGRAD) = range(11)
 
@@ -43,6 +44,7 @@ SIGNATURES = {
     "mlp_fwd": (_i, [_PD, _PL, _p, _p, _p, _z, _p, _p]),
     "mlp_bwd": (_i, [_PD, _PL, _p, _p, _z, _i, _f, _p, _p]),
     "mlp_train_step": (_i, [_PD, _PL, _p, _p, _p, _z, _f, _p, _p]),
+    "mlp_train_step_static": (_i, [_PD, _PL, _p, _p, _f, _p, _p]),
     "sgd_step": (_i, [_p, _p, _i, _p, _l, _f, _f, _p]),
     "cast_f32_bf16": (_i, [_p, _p, _l, _p]),
     "softmax_xent": (_i, [_i, _i, _p, _l, _p, _f, _p, _p, _p, _l, _i, _p]),

@@ -197,3 +197,15 @@ def test_conv_bwd_validates_before_enqueueing(lib):
     assert need > 0
     assert lib.conv3x3_tile_bwd(32, 56, 56, 256, 256, p, p, p, p, 1, p, p, need - 1, None) == m.IMBD_EWORKSPACE
     assert lib.mlp_status_string(-4) == lib.imbd_status_string(-4)
+
+
+def test_static_scratch_refuses_oversized_network_on_the_host(lib):
+    import paper_1712_04432_amd as m
+    net = m.MLP((9216, 4096, 4096, 1000), 2048, "bf16")
+    assert m.mlp_workspace_bytes(net) > m.IMBD_STATIC_SCRATCH_BYTES
+    p = ctypes.c_void_p(256)
+    layers = m._layers([{"w": _Fake(256), "w_lp": _Fake(512), "b": _Fake(768)}] * 3)
+    assert lib.mlp_train_step_static(net.desc, layers, p, p, 0.01, p, None) == m.IMBD_EWORKSPACE
+    assert b"static scratch" in lib.imbd_last_error()
+    bad = m.MLP((8, 0, 2), 4, "bf16")
+    assert lib.mlp_train_step_static(bad.desc, layers, p, p, 0.01, p, None) == m.IMBD_EINVAL
