@@ -605,7 +605,7 @@ def main():
 
     # the first warm-up step starts from the seeded state: kept for the comparison with the oracle
     first_dev = None
-    if args.warmup >= 1:
+    if args.warmup >= 1 and not args.no_cpu_baseline:
         step()
         torch.cuda.synchronize()
         first_dev = {"loss": loss.item(), "w": [l["w"].cpu().numpy() for l in layers],

@@ -258,7 +258,9 @@ enum imbd_option {
     IMBD_OPT_GEMM_CFG = 8,      /* tile configuration of the tiled template, -1 = planned (-1..3) */
     IMBD_OPT_GEMM_SPLITS = 9,   /* K split of the tiled template, 0 = planned */
     IMBD_OPT_CONV_NT = 10,      /* 0: the conv tile on the tiled template */
-    IMBD_OPT_COUNT = 11
+    IMBD_OPT_SKINNY_NB = 11,    /* samples per workgroup of the B <= 256 product kernel, in units
+                                   of 64 (1, 2 or 4), 0 = planned */
+    IMBD_OPT_COUNT = 12
 };
 /* Each option starts at the value of the environment variable named by
  * imbd_option_name(key) when the library is loaded (its default if unset or out of

@@ -33,6 +33,7 @@ const OptionDef kOptions[IMBD_OPT_COUNT] = {
     {"IMBD_GEMM_CFG", -1, -1, 3},        // tiled template's tile configuration (-1: planner)
     {"IMBD_GEMM_SPLITS", 0, 0, 4096},    // tiled template's K split (0: planner)
     {"IMBD_CONV_NT", 1, 0, 1},           // conv tile on the large-tile kernels
+    {"IMBD_SKINNY_NB", 0, 0, 4},         // skinny kernel's samples per workgroup / 64 (0: planner)
 };
 
 std::atomic<int> g_opt[IMBD_OPT_COUNT];
@@ -45,7 +46,7 @@ struct OptionInit {
       const char *e = getenv(d.env);
       if (e && *e) {
         const long x = strtol(e, nullptr, 10);
-        if (x >= d.lo && x <= d.hi) v = (int)x;
+        if (x >= d.lo && x <= d.hi && !(i == IMBD_OPT_SKINNY_NB && x == 3)) v = (int)x;
       }
       g_opt[i].store(v, std::memory_order_relaxed);
     }
@@ -70,7 +71,7 @@ int imbd_set_option(int key, int value) {
     return IMBD_EINVAL;
   }
   const OptionDef &d = kOptions[key];
-  if (value < d.lo || value > d.hi) {
+  if (value < d.lo || value > d.hi || (key == IMBD_OPT_SKINNY_NB && value == 3)) {
     set_error("option %s: value %d outside [%d, %d]", d.env, value, d.lo, d.hi);
     return IMBD_EINVAL;
   }

@@ -33,9 +33,25 @@ struct SkArgs {
   const uint16_t *B;  // activations: [N][ldb], k contiguous
   int64_t lda, ldb;
   int M, N, K;
-  int k_split, splits, tiles_m;
-  float *partial;     // [split][tile][N][64]: one contiguous block per workgroup
+  int k_split, splits, tiles_m, tiles_n;  // a workgroup: 64 rows x 64*NB samples x one K-range
+  float *partial;     // [split][tile][N][64]: one contiguous block per (split, row tile)
   int64_t tpitch, sstride;
+  // splits == 1 and fused: the store epilogue applied here instead of writing partials
+  int fused;
+  float alpha;
+  const float *bias;        // [M] or null
+  int relu;
+  const uint16_t *mask;     // bf16 [N][ldmask] or null: zero where !(mask > 0)
+  int64_t ldmask;
+  void *out;                // [N][ldo], bf16 (out_bf16) or fp32
+  int64_t ldo;
+  int out_bf16;
+  int vec;                  // out, mask and bias rows 8-byte (bf16) / 16-byte (fp32) aligned at every 4th m
+  // side job in one extra workgroup (the last): *aux_loss = aux_scale * sum of aux_rows
+  const float *aux_rows;
+  float *aux_loss;
+  int aux_n;
+  float aux_scale;
 };
 
 // Partial-sum layout: each workgroup's 64 x N tile is one contiguous block (a tile pitch
@@ -71,11 +87,17 @@ __global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int G = gridDim.x;
+  const int G = a.tiles_m * a.tiles_n * a.splits;  // product workgroups (an extra one carries aux)
+  if (a.aux_loss && (int)blockIdx.x == G) {
+    block_loss_mean(a.aux_n, a.aux_rows, a.aux_scale, a.aux_loss, reinterpret_cast<float *>(smem));
+    return;
+  }
   int b = blockIdx.x;
-  // consecutive logical blocks (the tiles of one K-range) on one XCD
+  // consecutive logical blocks on one XCD: the sample tiles of one row tile, then the row
+  // tiles of one K-range
   if ((G & 7) == 0) b = (b & 7) * (G >> 3) + (b >> 3);
-  const int split = b / a.tiles_m, m0 = (b - split * a.tiles_m) * SK_BM;
+  const int nt = b % a.tiles_n, mk = b / a.tiles_n;
+  const int split = mk / a.tiles_m, m0 = (mk - split * a.tiles_m) * SK_BM, n0 = nt * XROWS;
   const int klo = split * a.k_split, krange = min(a.K, klo + a.k_split) - klo;
   const int nsl = (krange + SK_KS - 1) / SK_KS;
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
@@ -93,7 +115,7 @@ __global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
     for (int q = 0; q < 4 * NB; ++q) {
       const int r = 8 * (4 * NB * xw + q) + (lane >> 3);
       const int c = (lane & 7) ^ swz_kc(r);
-      base[q] = (uint32_t)(((int64_t)r * a.ldb + klo + 8 * c) * 2);  // rows past N: out of range
+      base[q] = (uint32_t)(((int64_t)(n0 + r) * a.ldb + klo + 8 * c) * 2);  // rows past N: out of range
       kof[q] = 8 * c;
     }
     const uint32_t dst0 = ldsx + (uint32_t)(4 * NB * xw * 1024);
@@ -242,20 +264,84 @@ __global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
       }
   }
   lds_barrier();
-  // ---- partial tile out: one contiguous block, 16 threads per 256-byte row. Device-scope
-  // stores (sc1) write through the XCD's L2, so the partials do not sit there dirty until
-  // the end-of-kernel writeback (the AlexNet FC step is ~6 us faster than with default
-  // stores).
   const float *stg = reinterpret_cast<const float *>(smem);
-  float *dst = a.partial + (int64_t)split * a.sstride + (int64_t)(m0 / SK_BM) * a.tpitch;
-  const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(dst, 0, (int)(a.tpitch * 4), BUF_DW3);
   const int u = tid & 15;
+  if (!a.fused) {
+    // ---- partial tile out: the rows n0.. of one contiguous block, 16 threads per 256-byte
+    // row. Device-scope stores (sc1) write through the XCD's L2, so the partials do not sit
+    // there dirty until the end-of-kernel writeback (the AlexNet FC step is ~6 us faster
+    // than with default stores).
+    float *dst = a.partial + (int64_t)split * a.sstride + (int64_t)(m0 / SK_BM) * a.tpitch;
+    const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(dst, 0, (int)(a.tpitch * 4), BUF_DW3);
 #pragma unroll
-  for (int p = 0; p < 2 * NB; ++p) {
-    const int n = 32 * p + (tid >> 4);
-    if (n < a.N) {
-      const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + n * 64 + 4 * (u ^ (n & 15)));
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), prs, (uint32_t)((n * 64 + 4 * u) * 4), 0, CPOL_SC1);
+    for (int p = 0; p < 2 * NB; ++p) {
+      const int nl = 32 * p + (tid >> 4), n = n0 + nl;
+      if (n < a.N) {
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + nl * 64 + 4 * (u ^ (nl & 15)));
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), prs, (uint32_t)((n * 64 + 4 * u) * 4), 0, CPOL_SC1);
+      }
+    }
+    return;
+  }
+  {
+    // ---- whole K in this workgroup: out(m, n) = [mask > 0] * relu?(alpha * acc + bias[m]),
+    // four consecutive m of one sample per thread, the same arithmetic as the split reduce.
+    const int m = m0 + 4 * u;
+#pragma unroll
+    for (int p = 0; p < 2 * NB; ++p) {
+      const int nl = 32 * p + (tid >> 4), n = n0 + nl;
+      if (n < a.N && m < a.M) {
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + nl * 64 + 4 * (u ^ (nl & 15)));
+        const int cnt = min(4, a.M - m);
+        const bool vec = a.vec && cnt == 4;
+        float bb[4] = {0.f, 0.f, 0.f, 0.f};
+        bool keep[4] = {true, true, true, true};
+        if (vec) {
+          if (a.bias) {
+            const f32x4 t = *reinterpret_cast<const f32x4 *>(a.bias + m);
+            bb[0] = t[0]; bb[1] = t[1]; bb[2] = t[2]; bb[3] = t[3];
+          }
+          if (a.mask) {
+            const u32x2 mk = *reinterpret_cast<const u32x2 *>(a.mask + (int64_t)n * a.ldmask + m);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) keep[i] = bf16_to_f32((uint16_t)((mk[i >> 1] >> (16 * (i & 1))) & 0xffffu)) > 0.0f;
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (i < cnt) {
+              if (a.bias) bb[i] = a.bias[m + i];
+              if (a.mask) keep[i] = bf16_to_f32(a.mask[(int64_t)n * a.ldmask + m + i]) > 0.0f;
+            }
+        }
+        float x[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float y = a.alpha * v[i] + bb[i];
+          if (a.relu) y = y > 0.0f ? y : 0.0f;
+          x[i] = keep[i] ? y : 0.0f;
+        }
+        if (a.out_bf16) {
+          uint16_t *o = reinterpret_cast<uint16_t *>(a.out) + (int64_t)n * a.ldo + m;
+          if (vec) {
+            *reinterpret_cast<u32x2 *>(o) = u32x2{(uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16),
+                                                  (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16)};
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (i < cnt) o[i] = f32_to_bf16(x[i]);
+          }
+        } else {
+          float *o = reinterpret_cast<float *>(a.out) + (int64_t)n * a.ldo + m;
+          if (vec) {
+            *reinterpret_cast<f32x4 *>(o) = f32x4{x[0], x[1], x[2], x[3]};
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (i < cnt) o[i] = x[i];
+          }
+        }
+      }
     }
   }
 }
@@ -488,47 +574,74 @@ bool skinny_fits(const GemmProblem &p) {
          ((int64_t)256 * p.ldb + p.K + SK_KS) * 2 < ((int64_t)1 << 31);
 }
 
-// Splits: fill the chip, traded against the partials' traffic (each split writes an
-// fp32 M x N partial, which the reduce reads back). Modelled time of a split count: the
-// larger of the HBM time (W, the activations once, the partials written and read) and
-// the time of one workgroup (slabs at ~900 cycles each plus ~12k cycles of fill and
-// partial write-out), times the rounds of workgroups over 256 CUs. (Timed alone, several
-// products run faster on fewer workgroups with fewer splits, e.g. the 1000 x 4096
-// forward on 5 splits instead of 13; inside the training step those plans lose ~7 us,
-// so the model keeps the chip full.)
-void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
-  const int tiles = (p.M + SK_BM - 1) / SK_BM;
-  const double hbm = 5.0e12, clk = 2.1e9, slab_clk = 900.0, fill_clk = 12000.0;
-  int best_s = 1;
-  double best_t = 1e30;
-  const int forced = opt(IMBD_OPT_SKINNY_SPLITS);
-  for (int s = 1; s <= 64; ++s) {
-    const int ks = ((p.K + s - 1) / s + SK_KS - 1) / SK_KS * SK_KS;
-    if ((p.K + ks - 1) / ks != s) continue;
-    const int blocks = tiles * s;
-    if (blocks > 65535) break;
-    const double bytes = 2.0 * p.M * p.K + 2.0 * p.N * p.K + 8.0 * s * (double)p.M * p.N;
-    const int rounds = (blocks + 255) / 256;
-    const double t_cu = rounds * ((ks / SK_KS) * slab_clk + fill_clk) / clk;
-    // past 16 splits the reduce's threads wait on their loads round after round (four
-    // splits per round): ~0.6 us per extra round
-    const double t_red = 0.6e-6 * (double)((s + 3) / 4 > 4 ? (s + 3) / 4 - 4 : 0);
-    const double t = (bytes / hbm > t_cu ? bytes / hbm : t_cu) + t_red;
-    if (forced > 0 ? s == forced : t < best_t * 0.98) {
-      best_t = t;
-      best_s = s;
-    }
-  }
-  const int ks = ((p.K + best_s - 1) / best_s + SK_KS - 1) / SK_KS * SK_KS;
-  *k_split_out = ks;
-  *splits_out = (p.K + ks - 1) / ks;
+// Plan of a product: NB (64*NB samples per workgroup, tiles_n sample tiles) and the K
+// split. Modelled time of a plan: the rounds of workgroups over 256 CUs times one
+// workgroup's time (its 64-k slabs at a per-slab cost that grows with the bytes a slab
+// brings into LDS, plus a fixed cost of start-up and tile write-out, which is larger
+// for an fp32 partial tile than for the epilogue's output), bounded below by the HBM
+// time of W, the activations and the partials; a split plan also pays the reduce launch
+// (a slower reduce past four splits). Costs are the kernel's measured times on gfx950 in
+// the 9216-4096-4096-1000 step at B = 256 (cycles at 2.1 GHz): per slab 567 / 677 / 1090
+// cycles for 64 / 128 / 256 samples; fixed 7.6K (K whole, epilogue fused) and 7.1K /
+// 13.7K cycles (128 / 256 samples, partial tile); the reduce ~4.4 us plus 0.045 us per MB
+// of partials, ~3 us more past four splits.
+struct SkPlan {
+  int nb, tiles_n, splits, k_split;
+};
+
+static bool sk_fused_ok(const GemmProblem &p) {
+  return p.epi.mode == EPI_STORE && (p.epi.mask == nullptr || p.epi.mask_dtype == IMBD_BF16);
 }
 
-// Launches the product kernel (partials into ws); returns its arguments in *out.
-static int launch_skinny_product(const GemmProblem &p, void *ws, hipStream_t s, SkArgs *out) {
-  int splits, k_split;
-  skinny_plan(p, &splits, &k_split);
-  SkArgs g;
+static SkPlan sk_plan(const GemmProblem &p) {
+  const int tiles_m = (p.M + SK_BM - 1) / SK_BM;
+  const double hbm = 5.0e12, clk = 2.1e9;
+  const double slab_clk[5] = {0, 567.0, 677.0, 0, 1090.0};
+  const double fix_fused[5] = {0, 7600.0, 7600.0, 0, 9000.0};
+  const double fix_part[5] = {0, 7100.0, 7100.0, 0, 13700.0};
+  const int forced_s = opt(IMBD_OPT_SKINNY_SPLITS), forced_nb = opt(IMBD_OPT_SKINNY_NB);
+  const bool fusable = sk_fused_ok(p);
+  SkPlan best{4, 1, 1, p.K};
+  double best_t = 1e30;
+  for (int nb = 1; nb <= 4; nb *= 2) {
+    if (forced_nb > 0 ? nb != forced_nb : nb > nb_for(p.N)) continue;
+    const int tiles_n = (p.N + 64 * nb - 1) / (64 * nb);
+    for (int s = 1; s <= 64; ++s) {
+      const int ks = ((p.K + s - 1) / s + SK_KS - 1) / SK_KS * SK_KS;
+      if ((p.K + ks - 1) / ks != s) continue;
+      const int64_t blocks = (int64_t)tiles_m * tiles_n * s;
+      if (blocks > 65535) break;
+      const bool fused = s == 1 && fusable;
+      const double bytes = 2.0 * p.M * p.K + 2.0 * p.N * p.K + (fused ? 0.0 : 8.0 * s * (double)p.M * p.N);
+      const int64_t rounds = (blocks + 255) / 256;
+      const double t_cu = rounds * ((ks / SK_KS) * slab_clk[nb] + (fused ? fix_fused[nb] : fix_part[nb])) / clk;
+      // past 16 splits the reduce's threads wait on their loads round after round (four
+      // splits per round): ~0.6 us per extra round
+      const double t_red = fused ? 0.0
+                                 : 4.4e-6 + 0.045e-12 * 4.0 * s * (double)p.M * p.N + (s > 4 ? 3.0e-6 : 0.0) +
+                                       0.6e-6 * (double)((s + 3) / 4 > 4 ? (s + 3) / 4 - 4 : 0);
+      const double t = (bytes / hbm > t_cu ? bytes / hbm : t_cu) + t_red;
+      const bool pick = forced_s > 0 ? s == forced_s && (best_t == 1e30 || t < best_t) : t < best_t * 0.98;
+      if (pick) {
+        best_t = t;
+        best = SkPlan{nb, tiles_n, s, ks};
+      }
+    }
+  }
+  return best;
+}
+
+void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
+  const SkPlan pl = sk_plan(p);
+  *splits_out = pl.splits;
+  *k_split_out = pl.k_split;
+}
+
+// Launches the product kernel (partials into ws, or the epilogue applied in the kernel
+// when K is whole); returns its arguments in *out.
+static int launch_skinny_product(const GemmProblem &p, void *ws, hipStream_t s, SkArgs *out, bool allow_fused) {
+  const SkPlan pl = sk_plan(p);
+  SkArgs g{};
   g.A = reinterpret_cast<const uint16_t *>(p.A);
   g.B = reinterpret_cast<const uint16_t *>(p.B);
   g.lda = p.lda;
@@ -536,23 +649,44 @@ static int launch_skinny_product(const GemmProblem &p, void *ws, hipStream_t s, 
   g.M = p.M;
   g.N = p.N;
   g.K = p.K;
-  g.k_split = k_split;
-  g.splits = splits;
+  g.k_split = pl.k_split;
+  g.splits = pl.splits;
   g.tiles_m = (p.M + SK_BM - 1) / SK_BM;
+  g.tiles_n = pl.tiles_n;
   g.partial = reinterpret_cast<float *>(ws);
   g.tpitch = sk_tile_pitch(p.N);
   g.sstride = sk_split_pitch(p.M, p.N);
-  const int grid = g.tiles_m * splits;
-  const int nb = nb_for(p.N);
+  const Epilogue &e = p.epi;
+  g.fused = allow_fused && pl.splits == 1 && sk_fused_ok(p);
+  if (g.fused) {
+    auto al = [](const void *q, int a) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % a) == 0; };
+    g.alpha = e.alpha;
+    g.bias = e.bias;
+    g.relu = e.relu;
+    g.mask = reinterpret_cast<const uint16_t *>(e.mask);
+    g.ldmask = e.ldmask;
+    g.out = e.out;
+    g.ldo = e.ldo;
+    g.out_bf16 = e.out_dtype == IMBD_BF16 ? 1 : 0;
+    g.vec = al(e.bias, 16) && (e.mask == nullptr || (al(e.mask, 8) && e.ldmask % 4 == 0)) &&
+            (g.out_bf16 ? al(e.out, 8) : al(e.out, 16)) && e.ldo % 4 == 0;
+    if (p.aux_loss && p.aux_n > 0) {
+      g.aux_rows = p.aux_rows;
+      g.aux_loss = p.aux_loss;
+      g.aux_n = p.aux_n;
+      g.aux_scale = p.aux_scale;
+    }
+  }
+  const int grid = g.tiles_m * g.tiles_n * pl.splits + (g.aux_loss ? 1 : 0);
   {
     LaunchTimer t(p.kclass, p.layer, s);
     if (p.a_kc) {
-      if (nb == 1) hipLaunchKernelGGL((skinny_kernel<false, 1>), dim3(grid), dim3(512), 0, s, g);
-      else if (nb == 2) hipLaunchKernelGGL((skinny_kernel<false, 2>), dim3(grid), dim3(512), 0, s, g);
+      if (pl.nb == 1) hipLaunchKernelGGL((skinny_kernel<false, 1>), dim3(grid), dim3(512), 0, s, g);
+      else if (pl.nb == 2) hipLaunchKernelGGL((skinny_kernel<false, 2>), dim3(grid), dim3(512), 0, s, g);
       else hipLaunchKernelGGL((skinny_kernel<false, 4>), dim3(grid), dim3(512), 0, s, g);
     } else {
-      if (nb == 1) hipLaunchKernelGGL((skinny_kernel<true, 1>), dim3(grid), dim3(512), 0, s, g);
-      else if (nb == 2) hipLaunchKernelGGL((skinny_kernel<true, 2>), dim3(grid), dim3(512), 0, s, g);
+      if (pl.nb == 1) hipLaunchKernelGGL((skinny_kernel<true, 1>), dim3(grid), dim3(512), 0, s, g);
+      else if (pl.nb == 2) hipLaunchKernelGGL((skinny_kernel<true, 2>), dim3(grid), dim3(512), 0, s, g);
       else hipLaunchKernelGGL((skinny_kernel<true, 4>), dim3(grid), dim3(512), 0, s, g);
     }
   }
@@ -562,8 +696,8 @@ static int launch_skinny_product(const GemmProblem &p, void *ws, hipStream_t s, 
 
 int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
   SkArgs g;
-  int rc = launch_skinny_product(p, ws, s, &g);
-  if (rc != IMBD_OK) return rc;
+  int rc = launch_skinny_product(p, ws, s, &g, true);
+  if (rc != IMBD_OK || g.fused) return rc;
   const int splits = g.splits;
   SkReduceArgs r;
   r.partial = g.partial;
@@ -605,7 +739,7 @@ bool skinny_softmax_fits(const GemmProblem &p) {
 int run_skinny_softmax(const GemmProblem &p, void *ws, const int32_t *labels, float inv_batch, float *row_loss,
                        void *dz, int64_t lddz, int dz_dtype, hipStream_t s) {
   SkArgs g;
-  int rc = launch_skinny_product(p, ws, s, &g);
+  int rc = launch_skinny_product(p, ws, s, &g, false);
   if (rc != IMBD_OK) return rc;
   SkSoftmaxArgs a;
   a.partial = g.partial;
@@ -633,9 +767,10 @@ int run_skinny_softmax(const GemmProblem &p, void *ws, const int32_t *labels, fl
 }
 
 size_t skinny_ws_bytes(const GemmProblem &p) {
-  int splits, k_split;
-  skinny_plan(p, &splits, &k_split);
-  return (size_t)splits * (size_t)sk_split_pitch(p.M, p.N) * sizeof(float);
+  // a plan that leaves K whole still needs its one partial when the caller reduces it
+  // (the top layer's softmax pass reads the partials)
+  const SkPlan pl = sk_plan(p);
+  return (size_t)pl.splits * (size_t)sk_split_pitch(p.M, p.N) * sizeof(float);
 }
 
 }  // namespace imbd

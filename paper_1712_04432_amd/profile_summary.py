@@ -95,6 +95,35 @@ def mfma_utilisation(path: str, simds: int = 1024, xcds: int = 8):
     return sorted(out, key=lambda r: -r["dur_us"] * r["dispatches"])
 
 
+def counter_table(path: str, per_step_ref: str = ""):
+    """Per (kernel, grid, position in the step) group of a --pmc run: the median over its
+    dispatches of every counter collected (each summed over the instances rocprofv3
+    reports for a dispatch) and of the dispatch's duration."""
+    disp = collections.OrderedDict()
+    for r in csv.DictReader(open(path)):
+        d = int(r["Dispatch_Id"])
+        e = disp.setdefault(d, {"name": short_name(r["Kernel_Name"]), "grid": int(r["Grid_Size"]) // max(int(r["Workgroup_Size"]), 1),
+                                "wg": int(r["Workgroup_Size"]),
+                                "dur": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0, "c": {}})
+        e["c"][r["Counter_Name"]] = e["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    seq = list(disp.values())
+    steps = sum(1 for e in seq if per_step_ref and per_step_ref in e["name"])
+    groups = collections.defaultdict(list)
+    for e in seq:
+        groups[(e["name"], e["grid"], e["wg"])].append(e)
+    out = []
+    for (name, grid, wg), v in groups.items():
+        per = len(v) // steps if steps and len(v) % steps == 0 and len(v) >= steps else 1
+        for k in range(per):
+            sub = v[k::per]
+            label = name if per == 1 else f"{name} [{k + 1}/{per}]"
+            names = sorted({c for e in sub for c in e["c"]})
+            out.append({"kernel": label, "workgroups": grid, "wg_size": wg, "dispatches": len(sub),
+                        "dur_us": statistics.median(e["dur"] for e in sub),
+                        "counters": {c: statistics.median(e["c"].get(c, 0.0) for e in sub) for c in names}})
+    return sorted(out, key=lambda r: -r["dur_us"] * r["dispatches"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("trace")
@@ -108,7 +137,18 @@ def main():
     ap.add_argument("--mfma", action="store_true",
                     help="matrix-pipe utilisation per kernel of a --pmc run with SQ_VALU_MFMA_BUSY_CYCLES "
                          "and GRBM_GUI_ACTIVE")
+    ap.add_argument("--counters", action="store_true",
+                    help="every counter of a --pmc run, median per dispatch, per kernel and grid")
     a = ap.parse_args()
+    if a.counters:
+        rows = counter_table(a.trace, a.per_step_ref)[:a.top]
+        names = sorted({c for r in rows for c in r["counters"]})
+        print("| kernel | workgroups x size | dispatches | median us | " + " | ".join(names) + " |")
+        print("|---|---|---|---|" + "---|" * len(names))
+        for r in rows:
+            print(f"| `{r['kernel']}` | {r['workgroups']} x {r['wg_size']} | {r['dispatches']} | {r['dur_us']:.2f} | "
+                  + " | ".join(f"{r['counters'].get(c, 0.0):.4g}" for c in names) + " |")
+        return
     if a.mfma:
         print("| kernel | workgroups x size | dispatches | median us | GUI clock GHz | MFMA busy of GUI cycles | "
               "MFMA busy at 2.4 GHz |")

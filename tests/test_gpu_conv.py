@@ -62,8 +62,8 @@ def test_conv_tile_small(imbd, dev, N, H, W, Ci, Co, border):
     assert nrm_err(host(dx), oracle.conv3x3_dgrad(dyv, wv)) < 1e-5
     assert nrm_err(host(dw), oracle.conv3x3_wgrad(xv, dyv)) < 1e-5
     y16, dx16, _ = _run(imbd, dev, d, out_bf16=True)
-    assert nrm_err(host(y16), oracle.conv3x3_fwd(xv, wv)) < 2.0 ** -8
-    assert nrm_err(host(dx16), oracle.conv3x3_dgrad(dyv, wv)) < 2.0 ** -8
+    assert nrm_err(host(y16), oracle.conv3x3_fwd(xv, wv)) < 2.0 ** -8 + 1e-5
+    assert nrm_err(host(dx16), oracle.conv3x3_dgrad(dyv, wv)) < 2.0 ** -8 + 1e-5
 
 
 @pytest.mark.parametrize("border", [(False, False, False, False), (True, False, True, False)])

@@ -184,8 +184,10 @@ def test_alexnet_local_4x16_whole_grid(imbd, dev, layer):
         e = nrm_err(host(y), yref)
         assert e < TOL_EXACT_OPERANDS, e
     else:
-        e = nrm_err(host(y), oracle.round_bf16(oracle.relu(yref)))
-        assert e < 2.0 ** -8, e
+        # against the unrounded reference: one bf16 rounding (at most half a unit in the last
+        # place, 2^-8 of the largest value) plus the fp32 accumulation
+        e = nrm_err(host(y), oracle.relu(yref))
+        assert e < 2.0 ** -8 + TOL_EXACT_OPERANDS, e
     rdw, rdb = oracle.weight_grad(DY, X, 1.0 / B)
     ew, eb = nrm_err(dW, rdw), nrm_err(db, rdb)
     ex = 0.0
@@ -227,3 +229,4 @@ def test_alexnet_fc_b256_resume_is_bit_identical(imbd, dev):
     for a, b in zip(straight, layers):
         for k in ("w", "w_lp", "b"):
             assert torch.equal(a[k], b[k].cpu()), k
+

@@ -400,3 +400,4 @@ def test_alexnet_local_4x16_blocks_full_size(imbd, dev):
             rows = rng.choice(b, 8, replace=False)
             rdx = oracle.relu_mask(oracle.input_grad(W, DY[rows]), X[rows])
             assert nrm_err(host(dx)[rows], rdx) < 1e-4
+

@@ -14,7 +14,7 @@ from tests._util import bf16_values, dev_bf16_bits, host, nrm_err
 pytestmark = pytest.mark.gpu
 
 TOL_F32_OUT = 1e-5     # fp32 outputs of exact bf16 products, fp32 accumulation
-TOL_BF16_OUT = 2.0 ** -8
+TOL_BF16_OUT = 2.0 ** -8 + 1e-5   # one bf16 rounding of the largest value plus fp32 accumulation
 
 
 def _splits(n):
