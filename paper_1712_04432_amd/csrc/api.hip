@@ -460,7 +460,20 @@ static GemmProblem local_dx_problem(int dtype, int d_out_blk, int d_in, int b_bl
   p.lda = d_in;
   p.ldb = d_out_blk;
   p.kclass = IMBD_K_GEMM_DX;
+  p.b_kpad8 = dtype == IMBD_BF16 && d_out_blk % 8 != 0;  // the block is then always copied
   return p;
+}
+
+// A bf16 Delta_Y block whose rows are not whole 16-byte chunks (a 250-row block of the
+// 1000-wide top layer has a 500-byte pitch; any block of a width that is not a multiple
+// of 8) is copied once into the workspace with its rows padded with zeros to a multiple
+// of 8 elements, so that both backward products run on the large-tile kernels.
+static size_t local_dy_copy_bytes(int dtype, int d_out_blk, int b_blk) {
+  if (dtype != IMBD_BF16 || b_blk <= 0) return 0;
+  return align256((size_t)b_blk * (size_t)((d_out_blk + 7) / 8 * 8) * 2);
+}
+static bool local_dy_needs_copy(int dtype, int d_out_blk, const void *dy, int64_t lddy) {
+  return dtype == IMBD_BF16 && ((uintptr_t)dy % 16 != 0 || lddy % 8 != 0 || d_out_blk % 8 != 0);
 }
 
 size_t mlp_local_workspace_bytes(int which, int dtype, int d_out_blk, int d_in, int b_blk) {
@@ -468,7 +481,7 @@ size_t mlp_local_workspace_bytes(int which, int dtype, int d_out_blk, int d_in, 
   if (which == 0) return gemm_plan(local_fwd_problem(dtype, d_out_blk, d_in, b_blk)).ws_bytes;
   size_t a = gemm_plan(local_dw_problem(dtype, d_out_blk, d_in, b_blk)).ws_bytes;
   size_t b = gemm_plan(local_dx_problem(dtype, d_out_blk, d_in, b_blk)).ws_bytes;
-  return a > b ? a : b;
+  return local_dy_copy_bytes(dtype, d_out_blk, b_blk) + (a > b ? a : b);
 }
 
 static int check_grid(int P_r, int P_c, int d_out_blk, int d_in, int b_blk) {
@@ -515,8 +528,28 @@ int mlp_local_bwd(int dtype, int P_r, int P_c, int d_out_blk, int d_in, int b_bl
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const float scale = 1.0f / ((float)b_blk * (float)P_c > 0 ? (float)b_blk * (float)P_c : 1.0f);
+  // the copied Delta_Y block (if any) at the start of the workspace, the products' partial
+  // sums after it
+  const size_t cpy = local_dy_copy_bytes(dtype, d_out_blk, b_blk);
+  bool copied = false;
+  if (b_blk > 0 && local_dy_needs_copy(dtype, d_out_blk, dy_blk, lddy)) {
+    if (!ws || (uintptr_t)ws % 256 != 0 || ws_bytes < cpy)
+      FAIL(IMBD_EWORKSPACE, "the Delta_Y block needs an aligned copy: workspace of %zu bytes, 256-byte aligned, "
+                            "need at least %zu", ws_bytes, cpy);
+    const int64_t ld8 = (d_out_blk + 7) / 8 * 8;
+    TRY(run_repack_bf16(reinterpret_cast<const uint16_t *>(dy_blk), lddy, b_blk, d_out_blk,
+                        reinterpret_cast<uint16_t *>(ws), ld8, s));
+    dy_blk = ws;
+    lddy = ld8;
+    copied = true;
+  }
+  if (cpy > 0) {
+    ws = ws ? reinterpret_cast<char *>(ws) + cpy : nullptr;
+    ws_bytes = ws_bytes > cpy ? ws_bytes - cpy : 0;
+  }
   if (dx_part && b_blk > 0) {
     GemmProblem p = local_dx_problem(dtype, d_out_blk, d_in, b_blk);
+    p.b_kpad8 = copied;
     p.A = w_blk;
     p.lda = ldw;
     p.B = dy_blk;

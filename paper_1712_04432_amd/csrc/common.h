@@ -84,6 +84,9 @@ struct GemmProblem {
   float *aux_loss = nullptr;
   int aux_n = 0;
   float aux_scale = 1.0f;
+  // B's rows hold zeros from K up to K rounded up to 8 (a copied block): the B <= 256
+  // kernel may then take a K that is not a multiple of 8 when A is read by k-rows
+  bool b_kpad8 = false;
 };
 
 // Launch plan chosen for a product (a pure function of the shapes).
@@ -146,6 +149,9 @@ int run_bias_grad(int dtype, int M, int B, const void *dy, int64_t lddy, float a
 int run_sgd(float *w, uint16_t *w16, const float *g, int64_t n, float step, hipStream_t s,
             int layer);
 int run_cast(const float *src, uint16_t *dst, int64_t n, hipStream_t s);
+// dst[r][c] = src[r][c] for c < cols, 0 for cols <= c < ld_dst (bf16, any alignment of src)
+int run_repack_bf16(const uint16_t *src, int64_t ld_src, int rows, int cols, uint16_t *dst, int64_t ld_dst,
+                    hipStream_t s);
 int run_conv_fwd(int N, int H, int W, int Ci, int Co, const void *xp, const void *w, void *y,
                  int y_dtype, hipStream_t s);
 int run_conv_dgrad(int N, int H, int W, int Ci, int Co, const void *dyp, const void *w, void *dx,

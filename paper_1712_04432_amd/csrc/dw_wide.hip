@@ -3,7 +3,8 @@
 //   Delta_W[o][i] = sum_b Delta_Y[b][o] X[b][i]      (Sec. 1, K = the batch)
 //   w[o][i] -= lr * alpha * Delta_W[o][i];  w16[o][i] = bf16(w[o][i])   (Eq. (1))
 // (or, for the unfused and local backward passes, alpha * Delta_W stored as fp32). The
-// bias gradient (column sums of Delta_Y) is left to the column-sum kernel.
+// bias gradient (column sums of Delta_Y) comes from the workgroups of the first column
+// tile up to 512 samples, else from the column-sum kernel.
 //
 // At these batch sizes the product (2 x batch flops per weight) outweighs the update's
 // 10 bytes per weight, so the kernel takes the large-tile layout of the conv tile's
@@ -53,6 +54,11 @@ struct DlArgs {
   uint32_t w_bytes, w16_bytes;
   float lr, alpha;
   int tiles_o, tiles_i;
+  // bias gradient, db[o] = db_alpha * sum_b Delta_Y[b][o], by the workgroups of the first
+  // column tile (db_mode 0: none (a separate launch), 1: store db_out, 2: bias -= bias_lr * db)
+  int db_mode;
+  float db_alpha, bias_lr;
+  float *db_out, *bias;
 };
 
 __device__ __forceinline__ int dl_swz(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
@@ -64,7 +70,7 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
   constexpr int DRING = DL_ND * DL_DSLOT, XRING = DL_NX * DL_XSLOT;
   __shared__ __attribute__((aligned(1024))) char smem[DRING + XRING];
   static_assert(DRING + XRING <= 160 * 1024, "LDS");
-  static_assert(256 * DL_PITCH * 4 <= DRING + XRING, "staging");
+  static_assert(256 * DL_PITCH * 4 + 512 * 4 <= DRING + XRING, "staging and bias sums");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -204,6 +210,35 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
         for (int e = 0; e < 4; ++e)
           stg[(16 * (8 * wm + i) + 4 * kg + e) * DL_PITCH + 16 * (4 * wn + j) + fi] = acc[i][j][e];
   }
+  if (it == 0 && a.db_mode != 0) {
+    // ---- bias gradient of the tile's 256 rows o: thread t sums column o0 + t%256 over
+    // the samples of its half (t/256) in ascending order, the halves are added in order.
+    // The staged tile leaves the last 25 KB of LDS free.
+    __syncthreads();
+    float *part = reinterpret_cast<float *>(smem + 256 * DL_PITCH * 4);
+    const int col = tid & 255, half = tid >> 8, o = o0 + col;
+    const int kh = (a.K + 1) / 2, b0 = half * kh, b1 = min(a.K, b0 + kh);
+    float sum = 0.f;
+    if (o < a.N) {
+      const uint16_t *p = a.DY + o;
+      int b = b0;
+      for (; b + 8 <= b1; b += 8) {
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = bf16_to_f32(p[(int64_t)(b + q) * a.lddy]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) sum += v[q];
+      }
+      for (; b < b1; ++b) sum += bf16_to_f32(p[(int64_t)b * a.lddy]);
+    }
+    part[tid] = sum;
+    __syncthreads();
+    if (tid < 256 && o < a.N) {
+      const float db = a.db_alpha * (part[tid] + part[tid + 256]);
+      if (a.db_mode == 1) a.db_out[o] = db;
+      else a.bias[o] -= a.bias_lr * db;
+    }
+  }
   // ---- the update: thread (sub, ch) takes rows o0 + 16u + sub (u < 16), columns
   // i0 + 4ch .. +3, with all sixteen rows' masters in flight at once (eight: +1%; issued
   // by the loader waves before the last barrier, to overlap the MMA tail: +9%).
@@ -264,7 +299,7 @@ bool dw_wide_fits(const GemmProblem &p) {
       p.M <= 0 || p.N <= 0 || p.M % 8 || !al(p.A, 16) || !al(p.B, 16) || p.lda % 8 || p.ldb % 8 ||
       p.lda < p.M || p.ldb < p.N || !al(e.out, 16) || e.ldo % 4 || e.ldo < p.M)
     return false;
-  if (((int64_t)(p.K - 1) * p.lda + p.M) * 2 >= lim || ((int64_t)(p.K - 1) * p.ldb + p.N) * 2 >= lim ||
+  if (((int64_t)(p.K - 1) * p.lda + p.M) * 2 >= lim || ((int64_t)(p.K - 1) * p.ldb + (p.N + 7) / 8 * 8) * 2 >= lim ||
       ((int64_t)(p.N - 1) * e.ldo + p.M) * 4 >= lim)
     return false;
   if (e.mode == EPI_STORE) return e.out_dtype == IMBD_F32;  // alpha * Delta_W, fp32
@@ -279,7 +314,11 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   a.ldx = p.lda;
   a.lddy = p.ldb;
   a.x_bytes = (uint32_t)(((int64_t)(p.K - 1) * p.lda + p.M) * 2);
-  a.dy_bytes = (uint32_t)(((int64_t)(p.K - 1) * p.ldb + p.N) * 2);
+  // the descriptor ends at the last sample's row rounded up to whole 16-byte chunks: with
+  // a 16-byte aligned base and ldb a multiple of 8 that is still inside the caller's row,
+  // and a chunk that crossed a tighter end would read as zero whole (columns of the last
+  // sample dropped); columns past N only feed outputs that are not stored
+  a.dy_bytes = (uint32_t)(((int64_t)(p.K - 1) * p.ldb + (p.N + 7) / 8 * 8) * 2);
   a.M = p.M;
   a.N = p.N;
   a.K = p.K;
@@ -294,6 +333,14 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   a.alpha = p.epi.alpha;
   a.tiles_o = (p.N + 255) / 256;
   a.tiles_i = (p.M + 127) / 128;
+  // the bias gradient in the kernel up to 512 samples (a few microseconds of one column
+  // tile's workgroups); past that the column-sum kernel spreads it over more workgroups
+  const bool db_here = p.db_mode != 0 && p.K <= 512;
+  a.db_mode = db_here ? p.db_mode : 0;
+  a.db_alpha = p.db_alpha;
+  a.bias_lr = p.bias_lr;
+  a.db_out = p.db_out;
+  a.bias = p.bias;
   const int grid = (a.tiles_o * a.tiles_i + 7) / 8 * 8;
   {
     LaunchTimer t(p.kclass, p.layer, s);
@@ -301,7 +348,7 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
     else hipLaunchKernelGGL(dw_wide_kernel<false>, dim3(grid), dim3(512), 0, s, a);
   }
   int rc = check_launch("dw_wide");
-  if (rc != IMBD_OK || p.db_mode == 0) return rc;
+  if (rc != IMBD_OK || p.db_mode == 0 || db_here) return rc;
   return run_bias_grad(IMBD_BF16, p.N, p.K, p.B, p.ldb, p.db_alpha, p.db_mode == 1 ? p.db_out : nullptr,
                        p.db_mode == 2 ? p.bias : nullptr, p.bias_lr, s, p.layer);
 }

@@ -276,6 +276,26 @@ int run_sgd(float *w, uint16_t *w16, const float *g, int64_t n, float step, hipS
   return check_launch("sgd");
 }
 
+__global__ void __launch_bounds__(256)
+    repack_bf16_kernel(const uint16_t *__restrict__ src, int64_t ld_src, int rows, int cols,
+                       uint16_t *__restrict__ dst, int64_t ld_dst) {
+  const int64_t total = (int64_t)rows * ld_dst;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
+    const int64_t r = t / ld_dst, c = t - r * ld_dst;
+    dst[t] = c < cols ? src[r * ld_src + c] : (uint16_t)0;
+  }
+}
+
+int run_repack_bf16(const uint16_t *src, int64_t ld_src, int rows, int cols, uint16_t *dst, int64_t ld_dst,
+                    hipStream_t s) {
+  const int64_t total = (int64_t)rows * ld_dst;
+  if (total <= 0) return IMBD_OK;
+  const int64_t blocks = (total + 255) / 256;
+  hipLaunchKernelGGL(repack_bf16_kernel, dim3((unsigned)(blocks < 1024 ? blocks : 1024)), dim3(256), 0, s, src, ld_src,
+                     rows, cols, dst, ld_dst);
+  return check_launch("repack_bf16");
+}
+
 int run_cast(const float *src, uint16_t *dst, int64_t n, hipStream_t s) {
   if (n <= 0) return IMBD_OK;
   LaunchTimer t(IMBD_K_CAST, 0, s);

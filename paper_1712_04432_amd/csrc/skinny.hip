@@ -562,8 +562,10 @@ int nb_for(int N) { return N <= 64 ? 1 : N <= 128 ? 2 : 4; }
 }  // namespace
 
 bool skinny_dims_fit(const GemmProblem &p) {
+  // K a multiple of 8 (whole 16-byte chunks), or B's rows zero-padded past K with A read by
+  // k-rows (rows past K read as zero)
   return p.dtype == IMBD_BF16 && p.b_kc && p.epi.mode == EPI_STORE && p.db_mode == 0 && p.N >= 1 &&
-         p.N <= 256 && p.M >= 1 && p.K >= 8 && p.K % 8 == 0 && (p.a_kc || p.M % 8 == 0);
+         p.N <= 256 && p.M >= 1 && p.K >= 1 && (p.K % 8 == 0 || (p.b_kpad8 && !p.a_kc)) && (p.a_kc || p.M % 8 == 0);
 }
 
 bool skinny_fits(const GemmProblem &p) {
@@ -584,7 +586,7 @@ bool skinny_fits(const GemmProblem &p) {
 // the 9216-4096-4096-1000 step at B = 256 (cycles at 2.1 GHz): per slab 567 / 677 / 1090
 // cycles for 64 / 128 / 256 samples; fixed 7.6K (K whole, epilogue fused) and 7.1K /
 // 13.7K cycles (128 / 256 samples, partial tile); the reduce ~4.4 us plus 0.045 us per MB
-// of partials, ~3 us more past four splits.
+// of partials (0.116 us per MB past four splits, where four lanes share an output).
 struct SkPlan {
   int nb, tiles_n, splits, k_split;
 };
@@ -618,7 +620,7 @@ static SkPlan sk_plan(const GemmProblem &p) {
       // past 16 splits the reduce's threads wait on their loads round after round (four
       // splits per round): ~0.6 us per extra round
       const double t_red = fused ? 0.0
-                                 : 4.4e-6 + 0.045e-12 * 4.0 * s * (double)p.M * p.N + (s > 4 ? 3.0e-6 : 0.0) +
+                                 : 4.4e-6 + (s > 4 ? 0.116e-12 : 0.045e-12) * 4.0 * s * (double)p.M * p.N +
                                        0.6e-6 * (double)((s + 3) / 4 > 4 ? (s + 3) / 4 - 4 : 0);
       const double t = (bytes / hbm > t_cu ? bytes / hbm : t_cu) + t_red;
       const bool pick = forced_s > 0 ? s == forced_s && (best_t == 1e30 || t < best_t) : t < best_t * 0.98;
