@@ -9,15 +9,15 @@
 // At these batch sizes the product (2 x batch flops per weight) outweighs the update's
 // 10 bytes per weight, so the kernel takes the large-tile layout of the conv tile's
 // weight-gradient kernel (csrc/conv.hip), with the update done by the epilogue of each
-// tile (K is never split: the update needs the whole sum). A workgroup owns 256 output
+// tile (K is never split: the update needs the whole sum). A workgroup owns 256 (or 128) output
 // rows o x 128 input columns i; both operands are sample-major, so K = samples and both
 // fragments come from k-row slabs through the gfx950 LDS transpose read. Slabs of 64
 // samples:
-//  * waves 6-7 load the Delta_Y slab (64 samples x 256 columns, four 64-column quarters)
-//    through a 3-slot ring;
+//  * waves 6-7 load the Delta_Y slab (64 samples x 256 (128) columns, four (two) 64-column
+//    quarters) through a 3-slot ring;
 //  * waves 4-5 load the X slab (64 samples x 128 columns, two quarters) through a 4-slot
 //    ring;
-//  * waves 0-3 each accumulate 128 rows o x 64 columns i in registers.
+//  * waves 0-3 each accumulate 128 (64) rows o x 64 columns i in registers.
 // Samples past the batch are past the end of the buffer descriptors and read as zero;
 // columns past M or N only reach outputs that are not stored.
 // Then the tile goes through LDS ([o][i], fp32) and all eight waves update it: non-
@@ -33,7 +33,6 @@ namespace imbd {
 namespace {
 
 constexpr int DL_XSLOT = 64 * 256;   // 16 KB: 64 samples x 128 columns
-constexpr int DL_DSLOT = 64 * 512;   // 32 KB: 64 samples x 256 columns
 constexpr int DL_QSLOT = 64 * 128;   // one 64-column quarter of a slab
 constexpr int DL_NX = 4, DL_ND = 3;  // ring slots
 constexpr int DL_PITCH = 128 + 4;    // staging row pitch in floats
@@ -64,13 +63,17 @@ struct DlArgs {
 __device__ __forceinline__ int dl_swz(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
 
 // SGD: update the masters and the bf16 copy; else store alpha * Delta_W to w (fp32).
-template <bool SGD>
+// OH: output rows o per workgroup, 256 or 128 (half the tile where whole tiles would leave
+// most CUs idle in the last round).
+template <bool SGD, int OH>
 __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
   constexpr uint32_t OOB = 0x80000000u;
-  constexpr int DRING = DL_ND * DL_DSLOT, XRING = DL_NX * DL_XSLOT;
+  constexpr int NQ = OH / 64;                 // 64-column quarters of the Delta_Y slab
+  constexpr int DSLOT = 64 * 2 * OH;          // 64 samples x OH columns
+  constexpr int DRING = DL_ND * DSLOT, XRING = DL_NX * DL_XSLOT;
   __shared__ __attribute__((aligned(1024))) char smem[DRING + XRING];
   static_assert(DRING + XRING <= 160 * 1024, "LDS");
-  static_assert(256 * DL_PITCH * 4 + 512 * 4 <= DRING + XRING, "staging and bias sums");
+  static_assert(OH * DL_PITCH * 4 + 512 * 4 <= DRING + XRING, "staging and bias sums");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -83,20 +86,21 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
   const int gsz = min(DL_GM, a.tiles_o - og * DL_GM);
   L -= og * DL_GM * a.tiles_i;
   const int it = L / gsz, ot = og * DL_GM + (L - it * gsz);
-  const int o0 = ot * 256, i0 = it * 128;
+  const int o0 = ot * OH, i0 = it * 128;
   const int nsl = (a.K + 63) / 64;
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
   const uint32_t ldsd = lds0, ldsx = lds0 + DRING;
 
   if (wave >= 6) {
     // ---------------------------------------------------- Delta_Y loaders (6, 7)
-    // the wave's blocks: quarters 2dw, 2dw+1, k-rows 8g + lane/8 of the slab
+    // the wave's blocks: quarters (NQ/2) dw .. (NQ/2) dw + NQ/2 - 1, k-rows 8g + lane/8
+    constexpr int QN = 4 * NQ;  // 1 KB blocks per wave
     const int dw = wave - 6;
     const i32x4 rd = buf_rsrc(a.DY, a.dy_bytes);
-    uint32_t base[16], dst[16];
+    uint32_t base[QN], dst[QN];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int h = 2 * dw + (q >> 3), g = q & 7;
+    for (int q = 0; q < QN; ++q) {
+      const int h = (NQ / 2) * dw + (q >> 3), g = q & 7;
       const int r = 8 * g + (lane >> 3);
       const int c = (lane & 7) ^ dl_swz(r);
       base[q] = (uint32_t)(((int64_t)r * a.lddy + o0 + 64 * h + 8 * c) * 2);
@@ -104,14 +108,14 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
     }
     const uint32_t sstep = (uint32_t)(64 * a.lddy * 2);
     auto issue = [&](int S) {
-      const uint32_t slot = ldsd + (uint32_t)((S % DL_ND) * DL_DSLOT);
+      const uint32_t slot = ldsd + (uint32_t)((S % DL_ND) * DSLOT);
 #pragma unroll
-      for (int q = 0; q < 16; ++q) dma16(rd, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
+      for (int q = 0; q < QN; ++q) dma16(rd, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
     };
 #pragma unroll
     for (int S = 0; S < DL_ND - 1; ++S) issue(S);
     for (int S = 0; S < nsl; ++S) {
-      vm_barrier<16 * (DL_ND - 2)>();  // slab S landed: B_S
+      vm_barrier<QN * (DL_ND - 2)>();  // slab S landed: B_S
       issue(S + DL_ND - 1);            // into the slot of S-1
     }
     vm_barrier<0>();
@@ -142,15 +146,15 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
     vm_barrier<0>();
   } else {
     // --------------------------------------------------------------- MMA group
-    // wave (wm, wn): rows o 128wm.. (Delta_Y quarters 2wm, 2wm+1), columns i 64wn..
-    constexpr int FM = 8;
+    // wave (wm, wn): rows o (OH/2)wm.. (Delta_Y quarters (NQ/2)wm ..), columns i 64wn..
+    constexpr int FM = OH / 32;
     const int fi = lane & 15, kg = lane >> 4;
     const int wm = wave & 1, wn = wave >> 1;
     const int r = 8 * kg + (fi >> 2);
     uint32_t fa[FM], fx[4];
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-      const int mb = 8 * wm + i, h = mb >> 2, ib = mb & 3;
+      const int mb = FM * wm + i, h = mb >> 2, ib = mb & 3;
       const int c = (2 * ib + ((fi >> 1) & 1)) ^ dl_swz(r);
       fa[i] = (uint32_t)(h * DL_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
     }
@@ -193,7 +197,7 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
       mma(dv[0], xv[0]);
       __builtin_amdgcn_sched_barrier(0);
       lds_barrier();  // B_{S+1}
-      ds = ldsd + (uint32_t)(((S + 1) % DL_ND) * DL_DSLOT);
+      ds = ldsd + (uint32_t)(((S + 1) % DL_ND) * DSLOT);
       xs = ldsx + (uint32_t)(((S + 1) % DL_NX) * DL_XSLOT);
       read(ds, xs, 0, dv[0], xv[0]);  // past the last slab this reads a spent slot, unused
       __builtin_amdgcn_sched_barrier(0);
@@ -208,16 +212,17 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          stg[(16 * (8 * wm + i) + 4 * kg + e) * DL_PITCH + 16 * (4 * wn + j) + fi] = acc[i][j][e];
+          stg[(16 * (FM * wm + i) + 4 * kg + e) * DL_PITCH + 16 * (4 * wn + j) + fi] = acc[i][j][e];
   }
   if (it == 0 && a.db_mode != 0) {
-    // ---- bias gradient of the tile's 256 rows o: thread t sums column o0 + t%256 over
-    // the samples of its half (t/256) in ascending order, the halves are added in order.
-    // The staged tile leaves the last 25 KB of LDS free.
+    // ---- bias gradient of the tile's OH rows o: thread t sums column o0 + t%OH over the
+    // samples of its part (t/OH of 512/OH parts) in ascending order, the parts are added
+    // in order. The staged tile leaves LDS free past it.
     __syncthreads();
-    float *part = reinterpret_cast<float *>(smem + 256 * DL_PITCH * 4);
-    const int col = tid & 255, half = tid >> 8, o = o0 + col;
-    const int kh = (a.K + 1) / 2, b0 = half * kh, b1 = min(a.K, b0 + kh);
+    constexpr int NP = 512 / OH;
+    float *part = reinterpret_cast<float *>(smem + OH * DL_PITCH * 4);
+    const int col = tid % OH, pi = tid / OH, o = o0 + col;
+    const int kh = (a.K + NP - 1) / NP, b0 = min(a.K, pi * kh), b1 = min(a.K, b0 + kh);
     float sum = 0.f;
     if (o < a.N) {
       const uint16_t *p = a.DY + o;
@@ -233,13 +238,16 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
     }
     part[tid] = sum;
     __syncthreads();
-    if (tid < 256 && o < a.N) {
-      const float db = a.db_alpha * (part[tid] + part[tid + 256]);
+    if (tid < OH && o < a.N) {
+      float t = part[tid];
+#pragma unroll
+      for (int q = 1; q < NP; ++q) t += part[tid + q * OH];
+      const float db = a.db_alpha * t;
       if (a.db_mode == 1) a.db_out[o] = db;
       else a.bias[o] -= a.bias_lr * db;
     }
   }
-  // ---- the update: thread (sub, ch) takes rows o0 + 16u + sub (u < 16), columns
+  // ---- the update: thread (sub, ch) takes rows o0 + 16u + sub (u < OH/16), columns
   // i0 + 4ch .. +3, with all sixteen rows' masters in flight at once (eight: +1%; issued
   // by the loader waves before the last barrier, to overlap the MMA tail: +9%).
   const int ch = tid & 31, sub = tid >> 5;
@@ -257,20 +265,20 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
     lds_barrier();
     if (!colok) return;
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
+    for (int u = 0; u < OH / 16; ++u) {
       const f32x4 g = *reinterpret_cast<const f32x4 *>(stg + (16 * u + sub) * DL_PITCH + 4 * ch);
       __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a.alpha * g), rw, offw(u), 0, CPOL_COPY_ST);
     }
     return;
   }
-  f32x4 wold[16];
+  f32x4 wold[OH / 16];
   lds_barrier();
 #pragma unroll
-  for (int u = 0; u < 16; ++u)
+  for (int u = 0; u < OH / 16; ++u)
     wold[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, offw(u), 0, CPOL_MASTER_LD));
   if (!colok) return;
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
+  for (int u = 0; u < OH / 16; ++u) {
     const int ol = 16 * u + sub, o = o0 + ol;
     const f32x4 g = *reinterpret_cast<const f32x4 *>(stg + ol * DL_PITCH + 4 * ch);
     f32x4 nw;
@@ -331,7 +339,14 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   a.w16_bytes = sgd ? (uint32_t)(((int64_t)(p.N - 1) * p.epi.ldo2 + p.M) * 2) : 0;
   a.lr = p.epi.lr;
   a.alpha = p.epi.alpha;
-  a.tiles_o = (p.N + 255) / 256;
+  // 128-row tiles where they finish the launch in fewer tile-heights of time: the time
+  // of a launch is about its rounds of workgroups over 256 CUs times the tile height
+  // (256-row tiles keep a 10% preference: fewer, larger tiles amortise each tile's start)
+  const int64_t ti = (p.M + 127) / 128;
+  const int64_t t256 = (p.N + 255) / 256 * ti, t128 = (p.N + 127) / 128 * ti;
+  const bool half = ((t128 + 255) / 256) * 128 * 11 < ((t256 + 255) / 256) * 256 * 10;
+  const int oh = half ? 128 : 256;
+  a.tiles_o = (p.N + oh - 1) / oh;
   a.tiles_i = (p.M + 127) / 128;
   // the bias gradient in the kernel up to 512 samples (a few microseconds of one column
   // tile's workgroups); past that the column-sum kernel spreads it over more workgroups
@@ -344,8 +359,13 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   const int grid = (a.tiles_o * a.tiles_i + 7) / 8 * 8;
   {
     LaunchTimer t(p.kclass, p.layer, s);
-    if (sgd) hipLaunchKernelGGL(dw_wide_kernel<true>, dim3(grid), dim3(512), 0, s, a);
-    else hipLaunchKernelGGL(dw_wide_kernel<false>, dim3(grid), dim3(512), 0, s, a);
+    if (sgd) {
+      if (half) hipLaunchKernelGGL((dw_wide_kernel<true, 128>), dim3(grid), dim3(512), 0, s, a);
+      else hipLaunchKernelGGL((dw_wide_kernel<true, 256>), dim3(grid), dim3(512), 0, s, a);
+    } else {
+      if (half) hipLaunchKernelGGL((dw_wide_kernel<false, 128>), dim3(grid), dim3(512), 0, s, a);
+      else hipLaunchKernelGGL((dw_wide_kernel<false, 256>), dim3(grid), dim3(512), 0, s, a);
+    }
   }
   int rc = check_launch("dw_wide");
   if (rc != IMBD_OK || p.db_mode == 0 || db_here) return rc;
