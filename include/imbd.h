@@ -260,7 +260,9 @@ enum imbd_option {
     IMBD_OPT_CONV_NT = 10,      /* 0: the conv tile on the tiled template */
     IMBD_OPT_SKINNY_NB = 11,    /* samples per workgroup of the B <= 256 product kernel, in units
                                    of 64 (1, 2 or 4), 0 = planned */
-    IMBD_OPT_COUNT = 12
+    IMBD_OPT_DW_WIDE_DUAL = 12, /* the large-tile fused update with two workgroups per CU
+                                   (128-row tiles): 1 always, 0 never, -1 = planned (-1..1) */
+    IMBD_OPT_COUNT = 13
 };
 /* Each option starts at the value of the environment variable named by
  * imbd_option_name(key) when the library is loaded (its default if unset or out of

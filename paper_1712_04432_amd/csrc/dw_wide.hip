@@ -32,11 +32,9 @@
 namespace imbd {
 namespace {
 
-constexpr int DL_XSLOT = 64 * 256;   // 16 KB: 64 samples x 128 columns
-constexpr int DL_QSLOT = 64 * 128;   // one 64-column quarter of a slab
 constexpr int DL_NX = 4, DL_ND = 3;  // ring slots
 constexpr int DL_PITCH = 128 + 4;    // staging row pitch in floats
-constexpr int DL_GM = 8;             // o tiles per launch-order group
+constexpr int DL_GM = 8;             // o tiles per launch-order group (twice that on two workgroups per CU)
 constexpr int CPOL_MASTER_LD = 2;      // nt
 constexpr int CPOL_MASTER_ST = 2 | 16;  // nt, device scope
 constexpr int CPOL_COPY_ST = 16;        // device scope
@@ -65,85 +63,121 @@ __device__ __forceinline__ int dl_swz(int r) { return 2 * ((r >> 1) & 1) + 4 * (
 // SGD: update the masters and the bf16 copy; else store alpha * Delta_W to w (fp32).
 // OH: output rows o per workgroup, 256 or 128 (half the tile where whole tiles would leave
 // most CUs idle in the last round).
-template <bool SGD, int OH>
-__global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
+// DUAL (OH = 128): two workgroups per CU (80 KB of LDS and at most 128 registers a lane
+// each: 32-sample slabs in five-slot rings, fragments read one k-step at a time), so that
+// one workgroup's update streams while the other computes its product.
+template <bool SGD, int OH, bool DUAL>
+__global__ void __launch_bounds__(512, DUAL ? 2 : 1) dw_wide_kernel(DlArgs a) {
   constexpr uint32_t OOB = 0x80000000u;
   constexpr int NQ = OH / 64;                 // 64-column quarters of the Delta_Y slab
-  constexpr int DSLOT = 64 * 2 * OH;          // 64 samples x OH columns
-  constexpr int DRING = DL_ND * DSLOT, XRING = DL_NX * DL_XSLOT;
+  constexpr int SK = DUAL ? 32 : 64;          // samples per slab
+  constexpr int QB = SK / 8;                  // 1 KB blocks (8 samples x 128 B) per quarter
+  constexpr int QSLOT = SK * 128;             // one 64-column quarter of a slab
+  constexpr int DSLOT = SK * 2 * OH;          // SK samples x OH columns
+  constexpr int XSLOT = SK * 256;             // SK samples x 128 columns
+  constexpr int ND = DUAL ? 5 : DL_ND, NX = DUAL ? 5 : DL_NX;
+  constexpr int DRING = ND * DSLOT, XRING = NX * XSLOT;
   __shared__ __attribute__((aligned(1024))) char smem[DRING + XRING];
-  static_assert(DRING + XRING <= 160 * 1024, "LDS");
+  static_assert(!DUAL || OH == 128, "two workgroups per CU: 128-row tiles");
+  static_assert(DRING + XRING <= (DUAL ? 80 : 160) * 1024, "LDS");
   static_assert(OH * DL_PITCH * 4 + 512 * 4 <= DRING + XRING, "staging and bias sums");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   // grid padded to a multiple of 8; each XCD takes a contiguous range of the launch order,
-  // in which tiles come in groups of DL_GM o tiles x all i tiles (shared slabs in L2)
+  // in which tiles come in groups of GM o tiles x all i tiles (shared slabs in L2)
+  constexpr int GM = DUAL ? 2 * DL_GM : DL_GM;
   const int G = gridDim.x;
   int L = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
   if (L >= a.tiles_o * a.tiles_i) return;
-  const int og = L / (DL_GM * a.tiles_i);
-  const int gsz = min(DL_GM, a.tiles_o - og * DL_GM);
-  L -= og * DL_GM * a.tiles_i;
-  const int it = L / gsz, ot = og * DL_GM + (L - it * gsz);
+  const int og = L / (GM * a.tiles_i);
+  const int gsz = min(GM, a.tiles_o - og * GM);
+  L -= og * GM * a.tiles_i;
+  const int it = L / gsz, ot = og * GM + (L - it * gsz);
   const int o0 = ot * OH, i0 = it * 128;
-  const int nsl = (a.K + 63) / 64;
+  const int nsl = (a.K + SK - 1) / SK;
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
   const uint32_t ldsd = lds0, ldsx = lds0 + DRING;
+  // two workgroups per CU (SGD): each wave issues the loads of its masters as soon as its
+  // part of the product is done (the loader waves after their last slab landed, the MMA
+  // waves after their last MFMAs), so that they are in flight during the staging. (Loads
+  // issued by the loader waves right after their last slab's loads, before that slab
+  // landed, made the launch 3% slower.)
+  constexpr bool EARLY = SGD && DUAL;
+  // the update's share of each thread: rows o0 + 16u + sub (u < UR), columns i0 + 4ch .. +3
+  constexpr int US = 16, UR = OH / US;
+  const int ch = tid & 31, sub = tid >> 5;
+  const int i = i0 + 4 * ch;
+  const bool colok = i < a.M;
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(a.w, 0, (int)a.w_bytes, BUF_DW3);
+  const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(a.w16, 0, (int)a.w16_bytes, BUF_DW3);
+  // rows past N and columns past M: an offset past the descriptor (reads zero, no store)
+  auto offw = [&](int u) {
+    const int o = o0 + US * u + sub;
+    return (colok && o < a.N) ? (uint32_t)(((int64_t)o * a.ldw + i) * 4) : OOB;
+  };
+  f32x4 wold[UR];
+  auto load_masters = [&]() {
+#pragma unroll
+    for (int u = 0; u < UR; ++u)
+      wold[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, offw(u), 0, CPOL_MASTER_LD));
+  };
 
   if (wave >= 6) {
     // ---------------------------------------------------- Delta_Y loaders (6, 7)
     // the wave's blocks: quarters (NQ/2) dw .. (NQ/2) dw + NQ/2 - 1, k-rows 8g + lane/8
-    constexpr int QN = 4 * NQ;  // 1 KB blocks per wave
+    constexpr int QN = QB * NQ / 2;  // 1 KB blocks per wave
     const int dw = wave - 6;
     const i32x4 rd = buf_rsrc(a.DY, a.dy_bytes);
     uint32_t base[QN], dst[QN];
 #pragma unroll
     for (int q = 0; q < QN; ++q) {
-      const int h = (NQ / 2) * dw + (q >> 3), g = q & 7;
+      const int h = (NQ / 2) * dw + q / QB, g = q % QB;
       const int r = 8 * g + (lane >> 3);
       const int c = (lane & 7) ^ dl_swz(r);
       base[q] = (uint32_t)(((int64_t)r * a.lddy + o0 + 64 * h + 8 * c) * 2);
-      dst[q] = (uint32_t)(h * DL_QSLOT + g * 1024);
+      dst[q] = (uint32_t)(h * QSLOT + g * 1024);
     }
-    const uint32_t sstep = (uint32_t)(64 * a.lddy * 2);
+    const uint32_t sstep = (uint32_t)(SK * a.lddy * 2);
     auto issue = [&](int S) {
-      const uint32_t slot = ldsd + (uint32_t)((S % DL_ND) * DSLOT);
+      const uint32_t slot = ldsd + (uint32_t)((S % ND) * DSLOT);
 #pragma unroll
       for (int q = 0; q < QN; ++q) dma16(rd, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
     };
 #pragma unroll
-    for (int S = 0; S < DL_ND - 1; ++S) issue(S);
+    for (int S = 0; S < ND - 1; ++S) issue(S);
     for (int S = 0; S < nsl; ++S) {
-      vm_barrier<QN * (DL_ND - 2)>();  // slab S landed: B_S
-      issue(S + DL_ND - 1);            // into the slot of S-1
+      vm_barrier<QN * (ND - 2)>();  // slab S landed: B_S
+      issue(S + ND - 1);            // into the slot of S-1
     }
     vm_barrier<0>();
+    if constexpr (EARLY) load_masters();
   } else if (wave >= 4) {
     // --------------------------------------------------------- X loaders (4, 5)
     const int xw = wave - 4;
     const i32x4 rx = buf_rsrc(a.X, a.x_bytes);
-    uint32_t base[8], dst[8];
+    uint32_t base[QB], dst[QB];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
+    for (int q = 0; q < QB; ++q) {
       const int r = 8 * q + (lane >> 3);
       const int c = (lane & 7) ^ dl_swz(r);
       base[q] = (uint32_t)(((int64_t)r * a.ldx + i0 + 64 * xw + 8 * c) * 2);
-      dst[q] = (uint32_t)(xw * DL_QSLOT + q * 1024);
+      dst[q] = (uint32_t)(xw * QSLOT + q * 1024);
     }
-    const uint32_t sstep = (uint32_t)(64 * a.ldx * 2);
+    const uint32_t sstep = (uint32_t)(SK * a.ldx * 2);
     auto issue = [&](int S) {
-      const uint32_t slot = ldsx + (uint32_t)((S % DL_NX) * DL_XSLOT);
+      const uint32_t slot = ldsx + (uint32_t)((S % NX) * XSLOT);
 #pragma unroll
-      for (int q = 0; q < 8; ++q) dma16(rx, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
+      for (int q = 0; q < QB; ++q) dma16(rx, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
     };
 #pragma unroll
-    for (int S = 0; S < DL_NX - 1; ++S) issue(S);
+    for (int S = 0; S < NX - 1; ++S) issue(S);
     for (int S = 0; S < nsl; ++S) {
-      vm_barrier<8 * (DL_NX - 2)>();  // slab S landed: B_S
-      issue(S + DL_NX - 1);           // into the slot of S-1
+      vm_barrier<QB * (NX - 2)>();  // slab S landed: B_S
+      issue(S + NX - 1);           // into the slot of S-1
     }
     vm_barrier<0>();
+    if constexpr (EARLY) load_masters();
   } else {
     // --------------------------------------------------------------- MMA group
     // wave (wm, wn): rows o (OH/2)wm.. (Delta_Y quarters (NQ/2)wm ..), columns i 64wn..
@@ -156,12 +190,12 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
     for (int i = 0; i < FM; ++i) {
       const int mb = FM * wm + i, h = mb >> 2, ib = mb & 3;
       const int c = (2 * ib + ((fi >> 1) & 1)) ^ dl_swz(r);
-      fa[i] = (uint32_t)(h * DL_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
+      fa[i] = (uint32_t)(h * QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int c = (2 * j + ((fi >> 1) & 1)) ^ dl_swz(r);
-      fx[j] = (uint32_t)(wn * DL_QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
+      fx[j] = (uint32_t)(wn * QSLOT + r * 128 + c * 16 + 8 * (fi & 1));
     }
     f32x4 acc[FM][4];
 #pragma unroll
@@ -190,20 +224,33 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
     };
     uint32_t ds = ldsd, xs = ldsx;
     lds_barrier();  // B_0
-    read(ds, xs, 0, dv[0], xv[0]);
-    for (int S = 0; S < nsl; ++S) {
-      read(ds, xs, 1, dv[1], xv[1]);
-      __builtin_amdgcn_sched_barrier(0);
-      mma(dv[0], xv[0]);
-      __builtin_amdgcn_sched_barrier(0);
-      lds_barrier();  // B_{S+1}
-      ds = ldsd + (uint32_t)(((S + 1) % DL_ND) * DSLOT);
-      xs = ldsx + (uint32_t)(((S + 1) % DL_NX) * DL_XSLOT);
-      read(ds, xs, 0, dv[0], xv[0]);  // past the last slab this reads a spent slot, unused
-      __builtin_amdgcn_sched_barrier(0);
-      mma(dv[1], xv[1]);
-      __builtin_amdgcn_sched_barrier(0);
+    if constexpr (DUAL) {
+      // one k-step (the whole 32-sample slab) at a time (register budget of two workgroups
+      // per CU); the other workgroup's waves cover the read latency
+      for (int S = 0; S < nsl; ++S) {
+        read(ds, xs, 0, dv[0], xv[0]);
+        mma(dv[0], xv[0]);
+        lds_barrier();  // B_{S+1}
+        ds = ldsd + (uint32_t)(((S + 1) % ND) * DSLOT);
+        xs = ldsx + (uint32_t)(((S + 1) % NX) * XSLOT);
+      }
+    } else {
+      read(ds, xs, 0, dv[0], xv[0]);
+      for (int S = 0; S < nsl; ++S) {
+        read(ds, xs, 1, dv[1], xv[1]);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(dv[0], xv[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        lds_barrier();  // B_{S+1}
+        ds = ldsd + (uint32_t)(((S + 1) % ND) * DSLOT);
+        xs = ldsx + (uint32_t)(((S + 1) % NX) * XSLOT);
+        read(ds, xs, 0, dv[0], xv[0]);  // past the last slab this reads a spent slot, unused
+        __builtin_amdgcn_sched_barrier(0);
+        mma(dv[1], xv[1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
+    if constexpr (EARLY) load_masters();
     // ---- stage the tile as [o][i] fp32
     float *stg = reinterpret_cast<float *>(smem);
 #pragma unroll
@@ -247,39 +294,29 @@ __global__ void __launch_bounds__(512, 1) dw_wide_kernel(DlArgs a) {
       else a.bias[o] -= a.bias_lr * db;
     }
   }
-  // ---- the update: thread (sub, ch) takes rows o0 + 16u + sub (u < OH/16), columns
-  // i0 + 4ch .. +3, with all sixteen rows' masters in flight at once (eight: +1%; issued
-  // by the loader waves before the last barrier, to overlap the MMA tail: +9%).
-  const int ch = tid & 31, sub = tid >> 5;
-  const int i = i0 + 4 * ch;
-  const bool colok = i < a.M;
-  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(a.w, 0, (int)a.w_bytes, BUF_DW3);
-  const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(a.w16, 0, (int)a.w16_bytes, BUF_DW3);
-  // rows past N and columns past M: an offset past the descriptor (reads zero, no store)
-  auto offw = [&](int u) {
-    const int o = o0 + 16 * u + sub;
-    return (colok && o < a.N) ? (uint32_t)(((int64_t)o * a.ldw + i) * 4) : OOB;
-  };
+  // ---- the update: thread (sub, ch) takes rows o0 + US*u + sub (u < UR), columns
+  // i0 + 4ch .. +3, with all its rows' masters in flight at once. One workgroup per CU: the
+  // loads issued after the staging (eight rows in flight instead of sixteen: +1%; issued by
+  // the loader waves before the last barrier: +9%). Two per CU: issued before the staging
+  // (above; the loader waves alone doing the whole update, their loads issued during the
+  // product, was 3% slower).
   const float *stg = reinterpret_cast<const float *>(smem);
   if constexpr (!SGD) {
     lds_barrier();
     if (!colok) return;
 #pragma unroll
-    for (int u = 0; u < OH / 16; ++u) {
-      const f32x4 g = *reinterpret_cast<const f32x4 *>(stg + (16 * u + sub) * DL_PITCH + 4 * ch);
+    for (int u = 0; u < UR; ++u) {
+      const f32x4 g = *reinterpret_cast<const f32x4 *>(stg + (US * u + sub) * DL_PITCH + 4 * ch);
       __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a.alpha * g), rw, offw(u), 0, CPOL_COPY_ST);
     }
     return;
   }
-  f32x4 wold[OH / 16];
   lds_barrier();
-#pragma unroll
-  for (int u = 0; u < OH / 16; ++u)
-    wold[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, offw(u), 0, CPOL_MASTER_LD));
+  if constexpr (!EARLY) load_masters();
   if (!colok) return;
 #pragma unroll
-  for (int u = 0; u < OH / 16; ++u) {
-    const int ol = 16 * u + sub, o = o0 + ol;
+  for (int u = 0; u < UR; ++u) {
+    const int ol = US * u + sub, o = o0 + ol;
     const f32x4 g = *reinterpret_cast<const f32x4 *>(stg + ol * DL_PITCH + 4 * ch);
     f32x4 nw;
 #pragma unroll
@@ -344,7 +381,11 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   // (256-row tiles keep a 10% preference: fewer, larger tiles amortise each tile's start)
   const int64_t ti = (p.M + 127) / 128;
   const int64_t t256 = (p.N + 255) / 256 * ti, t128 = (p.N + 127) / 128 * ti;
-  const bool half = ((t128 + 255) / 256) * 128 * 11 < ((t256 + 255) / 256) * 256 * 10;
+  // two workgroups per CU for the fused update when its 128-row tiles take more than one
+  // round of the 256 CUs: one workgroup's update then streams while the other computes
+  const int dual_opt = opt(IMBD_OPT_DW_WIDE_DUAL);
+  const bool dual = sgd && (dual_opt == 1 || (dual_opt == -1 && t128 > 256));
+  const bool half = dual || ((t128 + 255) / 256) * 128 * 11 < ((t256 + 255) / 256) * 256 * 10;
   const int oh = half ? 128 : 256;
   a.tiles_o = (p.N + oh - 1) / oh;
   a.tiles_i = (p.M + 127) / 128;
@@ -359,12 +400,13 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   const int grid = (a.tiles_o * a.tiles_i + 7) / 8 * 8;
   {
     LaunchTimer t(p.kclass, p.layer, s);
-    if (sgd) {
-      if (half) hipLaunchKernelGGL((dw_wide_kernel<true, 128>), dim3(grid), dim3(512), 0, s, a);
-      else hipLaunchKernelGGL((dw_wide_kernel<true, 256>), dim3(grid), dim3(512), 0, s, a);
+    if (dual) hipLaunchKernelGGL((dw_wide_kernel<true, 128, true>), dim3(grid), dim3(512), 0, s, a);
+    else if (sgd) {
+      if (half) hipLaunchKernelGGL((dw_wide_kernel<true, 128, false>), dim3(grid), dim3(512), 0, s, a);
+      else hipLaunchKernelGGL((dw_wide_kernel<true, 256, false>), dim3(grid), dim3(512), 0, s, a);
     } else {
-      if (half) hipLaunchKernelGGL((dw_wide_kernel<false, 128>), dim3(grid), dim3(512), 0, s, a);
-      else hipLaunchKernelGGL((dw_wide_kernel<false, 256>), dim3(grid), dim3(512), 0, s, a);
+      if (half) hipLaunchKernelGGL((dw_wide_kernel<false, 128, false>), dim3(grid), dim3(512), 0, s, a);
+      else hipLaunchKernelGGL((dw_wide_kernel<false, 256, false>), dim3(grid), dim3(512), 0, s, a);
     }
   }
   int rc = check_launch("dw_wide");

@@ -118,7 +118,8 @@ def test_bf16_fused_update_matches_oracle(imbd, dev, dims, B):
 # the options that route the fused update past 256 samples
 _UPDATE_ROUTES = {"streamed": {"dw_wide_min_k": 100000},
                   "reload": {"dw_wide_min_k": 100000, "dw_stream": 0},
-                  "wide": {"dw_wide_min_k": 257}}
+                  "wide": {"dw_wide_min_k": 257},
+                  "wide_dual": {"dw_wide_min_k": 257, "dw_wide_dual": 1}}
 
 
 @pytest.mark.parametrize("route", sorted(_UPDATE_ROUTES))
@@ -127,7 +128,8 @@ def test_bf16_fused_update_every_kernel_past_256_samples(imbd, dev, dims, B, rou
     """Past 256 samples three kernels can apply the fused update: the persistent one with
     Delta_Y streamed in slabs (the default up to 384 samples), the persistent one with its
     resident Delta_Y block reloaded per 256-sample chunk, and the large-tile one (the
-    default past 384). Each is forced in turn, up to the persistent kernel's 2048 samples."""
+    default past 384) with one or two workgroups per CU. Each is forced in turn, up to the
+    persistent kernel's 2048 samples."""
     with imbd.options(**_UPDATE_ROUTES[route]):
         _check_fused_update(imbd, dev, dims, B)
 
