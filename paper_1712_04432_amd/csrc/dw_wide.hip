@@ -381,10 +381,10 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   // (256-row tiles keep a 10% preference: fewer, larger tiles amortise each tile's start)
   const int64_t ti = (p.M + 127) / 128;
   const int64_t t256 = (p.N + 255) / 256 * ti, t128 = (p.N + 127) / 128 * ti;
-  // two workgroups per CU for the fused update when its 128-row tiles take more than one
-  // round of the 256 CUs: one workgroup's update then streams while the other computes
+  // two workgroups per CU when the 128-row tiles take more than one round of the 256 CUs:
+  // one workgroup's update (or store) then streams while the other computes
   const int dual_opt = opt(IMBD_OPT_DW_WIDE_DUAL);
-  const bool dual = sgd && (dual_opt == 1 || (dual_opt == -1 && t128 > 256));
+  const bool dual = dual_opt == 1 || (dual_opt == -1 && t128 > 256);
   const bool half = dual || ((t128 + 255) / 256) * 128 * 11 < ((t256 + 255) / 256) * 256 * 10;
   const int oh = half ? 128 : 256;
   a.tiles_o = (p.N + oh - 1) / oh;
@@ -400,8 +400,10 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s) {
   const int grid = (a.tiles_o * a.tiles_i + 7) / 8 * 8;
   {
     LaunchTimer t(p.kclass, p.layer, s);
-    if (dual) hipLaunchKernelGGL((dw_wide_kernel<true, 128, true>), dim3(grid), dim3(512), 0, s, a);
-    else if (sgd) {
+    if (dual) {
+      if (sgd) hipLaunchKernelGGL((dw_wide_kernel<true, 128, true>), dim3(grid), dim3(512), 0, s, a);
+      else hipLaunchKernelGGL((dw_wide_kernel<false, 128, true>), dim3(grid), dim3(512), 0, s, a);
+    } else if (sgd) {
       if (half) hipLaunchKernelGGL((dw_wide_kernel<true, 128, false>), dim3(grid), dim3(512), 0, s, a);
       else hipLaunchKernelGGL((dw_wide_kernel<true, 256, false>), dim3(grid), dim3(512), 0, s, a);
     } else {

@@ -153,6 +153,8 @@ LOCAL_SHAPES = [
     # (forward split over K; Delta_X whole), and a forward split 8 ways
     (264, 1032, 777), (512, 4096, 300),
     (200, 1000, 128),
+    # 9 x 33 tiles of 128 x 128, ragged: the fp32 weight-gradient store on two workgroups per CU
+    (1032, 4104, 72),
 ]
 
 
