@@ -251,7 +251,7 @@ enum imbd_option {
     IMBD_OPT_WIDE_OFF = 3,      /* 1: forward / Delta_X products of B > 256 on the tiled template */
     IMBD_OPT_WIDE_SPLITS = 4,   /* K split of the B > 256 product kernel, 0 = planned */
     IMBD_OPT_DW_WIDE_MIN_K = 5, /* smallest batch whose fused update runs on the large-tile
-                                   kernel (default 385) */
+                                   kernel (default 257) */
     IMBD_OPT_DW_STREAM = 6,     /* 0: past 256 samples the persistent update kernel reloads its
                                    Delta_Y block per 256 samples instead of streaming it */
     IMBD_OPT_DW_GENERIC = 7,    /* 1: the fused update on the tiled template */

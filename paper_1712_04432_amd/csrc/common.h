@@ -132,7 +132,7 @@ int run_loss_mean(int B, const float *row_loss, float inv_batch, float *loss, hi
 // takes the problem, and the launch.
 bool dw_sgd_fits(const GemmProblem &p);
 int run_dw_sgd(const GemmProblem &p, hipStream_t s);
-// The weight gradient on large tiles (bf16; the SGD update past 384 samples or the fp32
+// The weight gradient on large tiles (bf16; the SGD update past 256 samples or the fp32
 // store of alpha * Delta_W at any batch, in each tile's epilogue, the bias gradient on
 // the column-sum kernel): whether it takes the problem, and the launch.
 bool dw_wide_fits(const GemmProblem &p);

@@ -1,4 +1,4 @@
-// Fused weight gradient + SGD update of a fully connected layer for batches above 384
+// Fused weight gradient + SGD update of a fully connected layer for batches above 256
 // samples (bf16 operands, fp32 masters):
 //   Delta_W[o][i] = sum_b Delta_Y[b][o] X[b][i]      (Sec. 1, K = the batch)
 //   w[o][i] -= lr * alpha * Delta_W[o][i];  w16[o][i] = bf16(w[o][i])   (Eq. (1))
@@ -334,9 +334,10 @@ __global__ void __launch_bounds__(512, DUAL ? 2 : 1) dw_wide_kernel(DlArgs a) {
 
 bool dw_wide_fits(const GemmProblem &p) {
   const Epilogue &e = p.epi;
-  // the fused update: batches above 384 (smaller ones run on the persistent kernel, which
-  // streams Delta_Y past 256 samples and is the faster of the two up to 384 on the AlexNet
-  // and VGG FC stacks); the fp32 store: any batch
+  // the fused update: batches above 256 (smaller ones run on the persistent kernel with its
+  // Delta_Y block resident, the faster of the two there on the AlexNet and VGG FC stacks;
+  // from 257 samples this kernel, with two workgroups per CU where the tiles take more than
+  // one round, beats the persistent one with Delta_Y streamed); the fp32 store: any batch
   const int min_k = e.mode == EPI_STORE ? 1 : opt(IMBD_OPT_DW_WIDE_MIN_K);
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const int64_t lim = (int64_t)1 << 31;  // bytes in one buffer descriptor

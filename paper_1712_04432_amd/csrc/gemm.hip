@@ -1018,7 +1018,7 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     return rc;
   }
   // A bf16 weight gradient runs on the large-tile kernel when stored as fp32 (any batch) or
-  // fused with the update past 384 samples; the fused update of a smaller batch on the
+  // fused with the update past 256 samples; the fused update of a smaller batch on the
   // persistent one.
   if (dw_wide_fits(p)) return run_dw_wide(p, s);
   if (dw_sgd_fits(p) && opt(IMBD_OPT_DW_GENERIC) == 0) return run_dw_sgd(p, s);

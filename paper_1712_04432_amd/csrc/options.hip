@@ -27,7 +27,7 @@ const OptionDef kOptions[IMBD_OPT_COUNT] = {
     {"IMBD_TOP_UNFUSED", 0, 0, 1},       // top layer's softmax in its own launch
     {"IMBD_WIDE_OFF", 0, 0, 1},          // forward / Delta_X at B > 256 on the tiled template
     {"IMBD_WIDE_SPLITS", 0, 0, 4096},    // wide-batch kernel's K split (0: planner)
-    {"IMBD_DW_WIDE_MIN_K", 385, 1, 1 << 30},  // smallest batch whose fused update is large-tile
+    {"IMBD_DW_WIDE_MIN_K", 257, 1, 1 << 30},  // smallest batch whose fused update is large-tile
     {"IMBD_DW_STREAM", 1, 0, 1},         // persistent update past 256 samples streams Delta_Y
     {"IMBD_DW_GENERIC", 0, 0, 1},        // fused update on the tiled template
     {"IMBD_GEMM_CFG", -1, -1, 3},        // tiled template's tile configuration (-1: planner)

@@ -126,10 +126,9 @@ _UPDATE_ROUTES = {"streamed": {"dw_wide_min_k": 100000},
 @pytest.mark.parametrize("dims,B", [((264, 128, 24), 300), ((1032, 264, 16), 777), ((2056, 520, 16), 2048)])
 def test_bf16_fused_update_every_kernel_past_256_samples(imbd, dev, dims, B, route):
     """Past 256 samples three kernels can apply the fused update: the persistent one with
-    Delta_Y streamed in slabs (the default up to 384 samples), the persistent one with its
-    resident Delta_Y block reloaded per 256-sample chunk, and the large-tile one (the
-    default past 384) with one or two workgroups per CU. Each is forced in turn, up to the
-    persistent kernel's 2048 samples."""
+    Delta_Y streamed in slabs, the persistent one with its resident Delta_Y block reloaded
+    per 256-sample chunk, and the large-tile one (the default) with one or two workgroups
+    per CU. Each is forced in turn, up to the persistent kernel's 2048 samples."""
     with imbd.options(**_UPDATE_ROUTES[route]):
         _check_fused_update(imbd, dev, dims, B)
 
