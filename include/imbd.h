@@ -262,7 +262,9 @@ enum imbd_option {
                                    of 64 (1, 2 or 4), 0 = planned */
     IMBD_OPT_DW_WIDE_DUAL = 12, /* the large-tile fused update with two workgroups per CU
                                    (128-row tiles): 1 always, 0 never, -1 = planned (-1..1) */
-    IMBD_OPT_COUNT = 13
+    IMBD_OPT_LOCAL_PAIR = 13,   /* 0: the local backward pass's Delta_X and Delta_W products in two
+                                   launches instead of one (default 1) */
+    IMBD_OPT_COUNT = 14
 };
 /* Each option starts at the value of the environment variable named by
  * imbd_option_name(key) when the library is loaded (its default if unset or out of

@@ -19,6 +19,7 @@
 #include <vector>
 
 #include "common.h"
+#include "local_pair.h"
 
 namespace imbd {
 
@@ -547,6 +548,21 @@ int mlp_local_bwd(int dtype, int P_r, int P_c, int d_out_blk, int d_in, int b_bl
     ws = ws ? reinterpret_cast<char *>(ws) + cpy : nullptr;
     ws_bytes = ws_bytes > cpy ? ws_bytes - cpy : 0;
   }
+  GemmProblem pw = local_dw_problem(dtype, d_out_blk, d_in, b_blk);
+  pw.A = x_blk;
+  pw.lda = ldx;
+  pw.B = dy_blk;
+  pw.ldb = lddy;
+  if (db_part) {
+    pw.db_mode = 1;
+    pw.db_out = db_part;
+    pw.db_alpha = scale;
+  }
+  pw.epi.mode = EPI_STORE;
+  pw.epi.alpha = scale;
+  pw.epi.out = dw_part;
+  pw.epi.ldo = lddw;
+  pw.epi.out_dtype = IMBD_F32;
   if (dx_part && b_blk > 0) {
     GemmProblem p = local_dx_problem(dtype, d_out_blk, d_in, b_blk);
     p.b_kpad8 = copied;
@@ -563,24 +579,13 @@ int mlp_local_bwd(int dtype, int P_r, int P_c, int d_out_blk, int d_in, int b_bl
     p.epi.out = dx_part;
     p.epi.ldo = lddx;
     p.epi.out_dtype = IMBD_F32;
+    // the two products are independent: one launch when both run on the large-tile
+    // kernels without partial sums
+    const int rc = run_local_dx_dw_pair(p, pw, ws, s);
+    if (rc != 1) return rc;
     TRY(gemm_run(p, ws, ws_bytes, s));
   }
-  GemmProblem p = local_dw_problem(dtype, d_out_blk, d_in, b_blk);
-  p.A = x_blk;
-  p.lda = ldx;
-  p.B = dy_blk;
-  p.ldb = lddy;
-  if (db_part) {
-    p.db_mode = 1;
-    p.db_out = db_part;
-    p.db_alpha = scale;
-  }
-  p.epi.mode = EPI_STORE;
-  p.epi.alpha = scale;
-  p.epi.out = dw_part;
-  p.epi.ldo = lddw;
-  p.epi.out_dtype = IMBD_F32;
-  return gemm_run(p, ws, ws_bytes, s);
+  return gemm_run(pw, ws, ws_bytes, s);
 }
 
 // ------------------------------------------------------------------------- conv tile

@@ -23,6 +23,8 @@
 #include <stdlib.h>
 
 #include "cdna4.h"
+#include "dw_wide_body.h"
+#include "local_pair.h"
 #include "loss_mean.h"
 
 namespace imbd {
@@ -75,24 +77,30 @@ __device__ __forceinline__ int swz_kc(int r) { return r & 7; }
 // conflict-free (2 LDS cycles per 512 B).
 __device__ __forceinline__ int swz_tr(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
 
+// Bytes of LDS a workgroup of the kernel uses.
+template <int NB>
+constexpr int sk_lds_bytes() { return SK_NX * 64 * NB * 128 + SK_NW * SK_WSLOT; }
+
 // NB: the workgroup covers 64*NB samples; MMA wave w takes NB m-blocks and four
-// 16-sample blocks.
+// 16-sample blocks. One workgroup's tile: bid is its index in the launch (the product's
+// workgroups come first), smem its LDS (sk_lds_bytes<NB>() bytes). A function of its own
+// so that a launch can also run it beside another product's workgroups.
 template <bool A_TR, int NB>
-__global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
+__device__ __forceinline__ void skinny_body(const SkArgs &a, char *smem, int bid) {
   constexpr uint32_t OOB = 0x80000000u;
   constexpr int XROWS = 64 * NB;
   constexpr int XSLOT = XROWS * 128;
   constexpr int XRING = SK_NX * XSLOT;
-  __shared__ __attribute__((aligned(1024))) char smem[XRING + SK_NW * SK_WSLOT];
+  static_assert(XRING + SK_NW * SK_WSLOT == sk_lds_bytes<NB>(), "LDS size");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = a.tiles_m * a.tiles_n * a.splits;  // product workgroups (an extra one carries aux)
-  if (a.aux_loss && (int)blockIdx.x == G) {
+  if (a.aux_loss && bid == G) {
     block_loss_mean(a.aux_n, a.aux_rows, a.aux_scale, a.aux_loss, reinterpret_cast<float *>(smem));
     return;
   }
-  int b = blockIdx.x;
+  int b = bid;
   // consecutive logical blocks on one XCD: the sample tiles of one row tile, then the row
   // tiles of one K-range
   if ((G & 7) == 0) b = (b & 7) * (G >> 3) + (b >> 3);
@@ -344,6 +352,26 @@ __global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
       }
     }
   }
+}
+
+template <bool A_TR, int NB>
+__global__ void __launch_bounds__(512, 1) skinny_kernel(SkArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[sk_lds_bytes<NB>()];
+  skinny_body<A_TR, NB>(a, smem, (int)blockIdx.x);
+}
+
+// One launch for two independent products of a local backward pass (App. A): the Delta_X
+// partial W^T Delta_Y on this kernel with K whole (workgroups 0 .. n_sk-1) and the Delta_W
+// partial Delta_Y^T X stored as fp32 on the large-tile kernel (workgroups from n_pad, a
+// multiple of 8, so that its launch order keeps its XCD mapping). Each workgroup runs one
+// of the two bodies, so each product computes exactly what its own launch would.
+template <int NB, int OH>
+__global__ void __launch_bounds__(512, 1) dx_dw_pair_kernel(SkArgs sk, DlArgs dl, int n_sk, int n_pad, int g_dl) {
+  constexpr int L1 = sk_lds_bytes<NB>(), L2 = dl_lds_bytes<OH, false>();
+  __shared__ __attribute__((aligned(1024))) char smem[L1 > L2 ? L1 : L2];
+  const int bid = (int)blockIdx.x;
+  if (bid < n_sk) skinny_body<true, NB>(sk, smem, bid);
+  else if (bid >= n_pad) dw_wide_body<false, OH, false>(dl, smem, bid - n_pad, g_dl);
 }
 
 struct SkReduceArgs {
@@ -641,8 +669,8 @@ void skinny_plan(const GemmProblem &p, int *splits_out, int *k_split_out) {
 
 // Launches the product kernel (partials into ws, or the epilogue applied in the kernel
 // when K is whole); returns its arguments in *out.
-static int launch_skinny_product(const GemmProblem &p, void *ws, hipStream_t s, SkArgs *out, bool allow_fused) {
-  const SkPlan pl = sk_plan(p);
+// The kernel's arguments for a problem and its plan; returns the number of workgroups.
+static int prepare_skinny(const GemmProblem &p, const SkPlan &pl, void *ws, bool allow_fused, SkArgs *out) {
   SkArgs g{};
   g.A = reinterpret_cast<const uint16_t *>(p.A);
   g.B = reinterpret_cast<const uint16_t *>(p.B);
@@ -679,7 +707,14 @@ static int launch_skinny_product(const GemmProblem &p, void *ws, hipStream_t s, 
       g.aux_scale = p.aux_scale;
     }
   }
-  const int grid = g.tiles_m * g.tiles_n * pl.splits + (g.aux_loss ? 1 : 0);
+  *out = g;
+  return g.tiles_m * g.tiles_n * pl.splits + (g.aux_loss ? 1 : 0);
+}
+
+static int launch_skinny_product(const GemmProblem &p, void *ws, hipStream_t s, SkArgs *out, bool allow_fused) {
+  const SkPlan pl = sk_plan(p);
+  SkArgs g;
+  const int grid = prepare_skinny(p, pl, ws, allow_fused, &g);
   {
     LaunchTimer t(p.kclass, p.layer, s);
     if (p.a_kc) {
@@ -773,6 +808,38 @@ size_t skinny_ws_bytes(const GemmProblem &p) {
   // (the top layer's softmax pass reads the partials)
   const SkPlan pl = sk_plan(p);
   return (size_t)pl.splits * (size_t)sk_split_pitch(p.M, p.N) * sizeof(float);
+}
+
+int run_local_dx_dw_pair(const GemmProblem &dx, const GemmProblem &dw, void *ws, hipStream_t s) {
+  constexpr int NOT_TAKEN = 1;
+  if (opt(IMBD_OPT_LOCAL_PAIR) == 0 || opt(IMBD_OPT_SKINNY_OFF) != 0) return NOT_TAKEN;
+  if (dx.M <= 0 || dx.N <= 0 || dw.M <= 0 || dw.N <= 0 || dx.aux_loss || !dx.b_kc || dx.a_kc) return NOT_TAKEN;
+  if (!skinny_fits(dx) || !sk_fused_ok(dx) || !dw_wide_fits(dw) || dw.epi.mode != EPI_STORE) return NOT_TAKEN;
+  const SkPlan pl = sk_plan(dx);
+  if (pl.splits != 1) return NOT_TAKEN;  // its reduce would follow the pair
+  // the large-tile product alone on two workgroups per CU (a launch of its own is faster)
+  // or with its bias on the column-sum kernel: not paired
+  DlArgs d;
+  int oh, g_dl;
+  bool dual;
+  dw_wide_prepare(dw, 0, &d, &oh, &dual, &g_dl);
+  if (dual || (dw.db_mode != 0 && d.db_mode == 0)) return NOT_TAKEN;
+  SkArgs g;
+  const int n_sk = prepare_skinny(dx, pl, ws, true, &g);
+  const int n_pad = (n_sk + 7) / 8 * 8;
+  dw_wide_prepare(dw, n_pad, &d, &oh, &dual, &g_dl);
+  const int grid = n_pad + g_dl;
+  {
+    LaunchTimer t(dw.kclass, dw.layer, s);
+    const int v = 4 * (oh == 256) + pl.nb;
+    if (v == 1) hipLaunchKernelGGL((dx_dw_pair_kernel<1, 128>), dim3(grid), dim3(512), 0, s, g, d, n_sk, n_pad, g_dl);
+    else if (v == 2) hipLaunchKernelGGL((dx_dw_pair_kernel<2, 128>), dim3(grid), dim3(512), 0, s, g, d, n_sk, n_pad, g_dl);
+    else if (v == 4) hipLaunchKernelGGL((dx_dw_pair_kernel<4, 128>), dim3(grid), dim3(512), 0, s, g, d, n_sk, n_pad, g_dl);
+    else if (v == 5) hipLaunchKernelGGL((dx_dw_pair_kernel<1, 256>), dim3(grid), dim3(512), 0, s, g, d, n_sk, n_pad, g_dl);
+    else if (v == 6) hipLaunchKernelGGL((dx_dw_pair_kernel<2, 256>), dim3(grid), dim3(512), 0, s, g, d, n_sk, n_pad, g_dl);
+    else hipLaunchKernelGGL((dx_dw_pair_kernel<4, 256>), dim3(grid), dim3(512), 0, s, g, d, n_sk, n_pad, g_dl);
+  }
+  return check_launch("dx_dw_pair");
 }
 
 }  // namespace imbd

@@ -218,6 +218,44 @@ def test_local_bwd_parity(imbd, dev, dtype, shape):
     assert nrm_err(host(dx), oracle.input_grad(W, DY)) < 1e-5
 
 
+# (d_out block, d_in, samples): the 4 x 16 grid's layer-3 and layer-2 blocks, ragged ones, one
+# with 200 samples (128-sample workgroups), and ones whose Delta_W cannot take the large-tile
+# kernel (d_in not a multiple of 8), which keep two launches
+PAIR_SHAPES = [(250, 4096, 64), (1024, 4096, 64), (130, 200, 70), (264, 1032, 200), (3, 8, 5), (37, 100, 13)]
+
+
+@pytest.mark.parametrize("shape", PAIR_SHAPES)
+def test_local_bwd_one_launch_matches_two(imbd, dev, shape):
+    """The local backward pass's Delta_X and Delta_W partials are independent products; when
+    both run on the large-tile kernels without partial sums they share one launch, each
+    workgroup running one kernel's body, so every bit equals what two launches give. The
+    launch count of the Delta_X kernel class shows which route ran."""
+    import torch
+    dout, din, b = shape
+    _flush(f"local_bwd one launch vs two {shape}")
+    d, W, X, DY = _local_inputs(dout, din, b, "bf16", seed=5)
+    wd, xd, dyd = _to_dev(d, "w", "bf16", dev), _to_dev(d, "x", "bf16", dev), _to_dev(d, "dy", "bf16", dev)
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(1, imbd.IMBD_BF16, dout, din, b), 16),
+                     dtype=torch.uint8, device=dev)
+    out = {}
+    for pair in (1, 0):
+        dw = torch.full((dout, din), 7.0, device=dev)
+        db = torch.full((dout,), 7.0, device=dev)
+        dx = torch.full((b, din), 7.0, device=dev)
+        with imbd.options(local_pair=pair):
+            imbd.timing_begin(imbd.IMBD_K_GEMM_DX, -1, 16)
+            imbd.mlp_local_bwd(wd, dyd, xd, dw, 4, 16, db_part=db, dx_part=dx, mask_relu=True, ws=ws)
+            n_dx, _ = imbd.timing_end()
+        torch.cuda.synchronize()
+        out[pair] = (host(dw), host(db), host(dx), n_dx)
+    paired = din % 8 == 0
+    assert out[1][3] == (0 if paired else 1) and out[0][3] == 1, (out[1][3], out[0][3])
+    for a, c in zip(out[1][:3], out[0][:3]):
+        assert np.array_equal(a, c)
+    rdw, rdb, rdx = oracle.local_bwd(W, DY, X, 1.0 / (b * 16), mask_src=X)
+    assert nrm_err(out[1][0], rdw) < 1e-5 and nrm_err(out[1][1], rdb) < 1e-5 and nrm_err(out[1][2], rdx) < 1e-5
+
+
 def test_local_fwd_strided_views(imbd, dev):
     """Blocks passed as views of a larger array (leading dimension > row length)."""
     import torch
