@@ -953,8 +953,9 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     return IMBD_EINVAL;
   }
   const GemmPlan pl = gemm_plan(p);
-  if (p.aux_loss && (pl.cfg != PLAN_SKINNY || p.M <= 0 || p.N <= 0)) {
-    // only the skinny reduce carries the side job; elsewhere it gets its own launch
+  if (p.aux_loss && ((pl.cfg != PLAN_SKINNY && pl.cfg != PLAN_WIDE) || p.M <= 0 || p.N <= 0)) {
+    // the skinny-batch launches and the wide-batch product carry the side job; elsewhere
+    // it gets its own launch
     GemmProblem q = p;
     q.aux_loss = nullptr;
     const int rc = gemm_run(q, ws, ws_bytes, s);

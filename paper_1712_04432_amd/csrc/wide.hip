@@ -28,6 +28,7 @@
 #include <stdlib.h>
 
 #include "cdna4.h"
+#include "loss_mean.h"
 
 namespace imbd {
 namespace {
@@ -54,6 +55,12 @@ struct WdArgs {
   Epilogue epi;                             // finish when splits == 1
   float *partial;                           // [split][n][ldp] fp32 when splits > 1
   int64_t ldp, sstride;
+  int gmain;                                // product workgroups (a multiple of 8)
+  // side job in one extra workgroup (the last): *aux_loss = aux_scale * sum of aux_rows
+  const float *aux_rows;
+  float *aux_loss;
+  int aux_n;
+  float aux_scale;
 };
 
 __device__ __forceinline__ int wd_swz_kc(int r) { return r & 7; }
@@ -73,10 +80,14 @@ __global__ void __launch_bounds__(WD_NT, 1) wide_kernel(WdArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // The grid is padded to a multiple of 8 and each XCD takes a contiguous range of the
-  // launch order, in which the tiles of one split come in groups of WD_GM m tiles x all
-  // sample tiles: the workgroups resident on an XCD share weight and sample slabs in L2.
-  const int G = gridDim.x;
+  if (a.aux_loss && (int)blockIdx.x == a.gmain) {
+    block_loss_mean(a.aux_n, a.aux_rows, a.aux_scale, a.aux_loss, reinterpret_cast<float *>(smem));
+    return;
+  }
+  // The product's grid is padded to a multiple of 8 and each XCD takes a contiguous range
+  // of the launch order, in which the tiles of one split come in groups of WD_GM m tiles x
+  // all sample tiles: the workgroups resident on an XCD share weight and sample slabs in L2.
+  const int G = a.gmain;
   int L = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
   const int per_split = a.tiles_m * a.tiles_n;
   if (L >= per_split * a.splits) return;
@@ -384,7 +395,12 @@ int run_wide(const GemmProblem &p, float *partial, int64_t ldp, int64_t sstride,
   a.partial = partial;
   a.ldp = ldp;
   a.sstride = sstride;
-  const int grid = (a.tiles_m * a.tiles_n * a.splits + 7) / 8 * 8;
+  a.gmain = (a.tiles_m * a.tiles_n * a.splits + 7) / 8 * 8;
+  a.aux_rows = p.aux_rows;
+  a.aux_loss = p.aux_n > 0 ? p.aux_loss : nullptr;
+  a.aux_n = p.aux_n;
+  a.aux_scale = p.aux_scale;
+  const int grid = a.gmain + (a.aux_loss ? 1 : 0);
   {
     LaunchTimer t(p.kclass, p.layer, s);
     if (p.a_kc) hipLaunchKernelGGL(wide_kernel<false>, dim3(grid), dim3(WD_NT), 0, s, a);
