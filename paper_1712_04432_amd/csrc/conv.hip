@@ -4,18 +4,19 @@
 // channels, as implicit GEMMs on the zero-padded (H+2) x (W+2) grid:
 //   forward   D(P, o) = sum_{tap, c} x_pad[P + r*(W+2) + s][c] * W[o][tap][c]
 //   input grad D(P, c) = sum_{tap, o} dy_pad[P + (2-r)*(W+2) + 2-s][o] * W[o][tap][c]
-// with tap = 3r + s and P a position of the padded grid; D(P, .) is the output at the
-// interior position of P when P's row and column are inside the tile, and is dropped
-// otherwise. Each tap is a row shift of a dense [positions][channels] matrix, so a k-slab
-// (64 channels of one tap) of the activation operand is 64 contiguous channels of shifted
-// rows.
+// with tap = 3r + s and P = (n (H+2) + h) (W+2) + w the row of the padded grid whose
+// D(P, .) is the output at position (n, h, w). Each tap is a row shift of a dense
+// [positions][channels] matrix, so a k-slab (64 channels of one tap) of the activation
+// operand is 64 contiguous channels of shifted rows.
 //
 // The products are MFMA-bound (2 x 9 x C flops per output), so a workgroup owns a large
-// tile: 128 positions x all 256 channels over the whole K = 9 C (no split, no partials;
-// the epilogue writes the outputs). The kernel keeps the layout of the skinny-batch kernel
-// (csrc/skinny.hip): both operands travel through LDS in 64-k slabs written by buffer
-// loads that go straight to LDS in whole 128-byte lines, loader waves with their own
-// memory counters, one barrier per slab, XOR-swizzled 16-byte chunks:
+// tile: 128 output positions x all 256 channels over the whole K = 9 C (no split, no
+// partials; the epilogue writes the outputs). With one workgroup per CU, the tiles of a
+// short last round run as two 128-channel halves each (the loader and MMA waves of the
+// other half only keep the slab barriers). The kernel keeps the layout of the skinny-batch
+// kernel (csrc/skinny.hip): both operands travel through LDS in 64-k slabs written by
+// buffer loads that go straight to LDS in whole 128-byte lines, loader waves with their
+// own memory counters, one barrier per slab, XOR-swizzled 16-byte chunks:
 //  * waves 8-9 stream the activation slab (128 shifted rows x 128 B) through a 4-slot ring;
 //  * waves 10-11 stream the weight slab (256 channels x 64 k) through a 3-slot ring: rows
 //    of W for the forward pass, k-rows of W (64 output channels of one tap x 256 input
@@ -23,7 +24,7 @@
 //    come from the gfx950 LDS transpose read;
 //  * waves 0-7, two per SIMD, each accumulate 64 positions x 64 channels in registers.
 // After the last slab the tile goes through LDS ([position][channel], fp32) and is written
-// as whole 512-byte (bf16) or 1 KB (fp32) rows of the interior positions.
+// as whole 512-byte (bf16) or 1 KB (fp32) output rows.
 
 #include <stdlib.h>
 
@@ -41,14 +42,16 @@ constexpr int CV_ASLOT = CV_BM * 128;  // 16 KB
 constexpr int CV_WSLOT = CV_BN * 128;  // 32 KB
 constexpr int CV_QSLOT = 64 * 128;     // one 64-channel quarter of a transposed weight slab
 constexpr int CV_PITCH = CV_BN + 4;    // staging row pitch in floats (1040 B)
+constexpr int CV_CUS = 256;            // compute units of the chip: one workgroup each per round
 
 struct CvArgs {
   const uint16_t *act;  // x_pad (forward) or dy_pad (input gradient): [N][H+2][W+2][Ck]
   const uint16_t *w;    // [C_out][3][3][C_in]
   void *out;            // [N][H][W][256]
   int out_bf16;
-  int H, W, Ck, Cw;     // Ck: channels of act (the reduction); Cw: C_in (the W row's channel stride)
-  int M, tiles;         // positions computed (up to the last interior one), tiles of 128
+  int N, H, W, Ck, Cw;  // Ck: channels of act (the reduction); Cw: C_in (the W row's channel stride)
+  int M, tiles;         // output positions N*H*W, tiles of 128 of them
+  int tfull, gfull;     // tiles run whole (the first tfull), their workgroups (a multiple of 8)
 };
 
 __device__ __forceinline__ int cv_swz_kc(int r) { return r & 7; }
@@ -72,13 +75,22 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // the grid is padded to a multiple of 8; consecutive tiles (which share shifted
-  // activation rows) run on one XCD
-  const int G = gridDim.x;
-  const int b = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+  // The first gfull workgroups take whole tiles (padded to a multiple of 8; consecutive
+  // tiles, which share shifted activation rows, run on one XCD). The workgroups after
+  // them take the last tiles in 128-channel halves, two per tile, so that the chip's last
+  // round of workgroups is a short one.
+  int b, hc = -1;
+  if ((int)blockIdx.x < a.gfull) {
+    b = (int)((blockIdx.x & 7) * (a.gfull >> 3) + (blockIdx.x >> 3));
+    if (b >= a.tfull) return;
+  } else {
+    const int j = (int)blockIdx.x - a.gfull;
+    b = a.tfull + (j >> 1);
+    hc = j & 1;
+  }
   if (b >= a.tiles) return;
   const int m0 = b * BM;
-  const int Wp = a.W + 2;
+  const int Hp = a.H + 2, Wp = a.W + 2;
   const int nsl = 9 * a.Ck / CV_KS;
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
   const uint32_t ldsw = lds0, ldsa = lds0 + WRING;
@@ -92,7 +104,8 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
 
   if (wave >= NMW + 2) {
     // --------------------------------------------------------------- weight loaders
-    const int ww = wave - NMW - 2;
+    const int ww = wave - NMW - 2;  // loads the slab rows of channels 128 ww .. 128 ww + 127
+    const bool on = hc < 0 || ww == hc;
     const i32x4 rw = buf_rsrc(a.w, (uint32_t)((int64_t)9 * a.Ck * CV_BN * 2));
     uint32_t base[16];
     uint32_t dst[16];
@@ -115,6 +128,7 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
       }
     }
     auto issue = [&](int S) {
+      if (!on) return;  // a half tile's other channels: no loads, the same barriers
       const uint32_t slot = ldsw + (uint32_t)((S % CV_NW) * CV_WSLOT);
       uint32_t off = OOB;
       if (S < nsl) {
@@ -138,16 +152,23 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
     vm_barrier<0>();
   } else if (wave >= NMW) {
     // ----------------------------------------------------------- activation loaders
-    // BM rows m0.. shifted by the slab's tap; rows past the tensor read as zero. Wave aw
-    // fills the 1 KB blocks FM*aw .. FM*aw + FM-1 (8 rows each).
+    // The rows of the tile's BM output positions in the padded grid, shifted by the slab's
+    // tap; positions past the last one read as zero. Wave aw fills the 1 KB blocks
+    // FM*aw .. FM*aw + FM-1 (8 rows each).
     const int aw = wave - NMW;
-    const i32x4 ra = buf_rsrc(a.act, (uint32_t)((int64_t)(a.M + 2 * Wp + 2) * a.Ck * 2));
+    const i32x4 ra = buf_rsrc(a.act, (uint32_t)((int64_t)a.N * Hp * Wp * a.Ck * 2));
     uint32_t base[FM];
 #pragma unroll
     for (int q = 0; q < FM; ++q) {
       const int r = 8 * (FM * aw + q) + (lane >> 3);
       const int c = (lane & 7) ^ cv_swz_kc(r);
-      base[q] = (uint32_t)(((int64_t)(m0 + r) * a.Ck + 8 * c) * 2);
+      const int p = m0 + r;
+      uint32_t bq = OOB;  // OOB + any slab offset stays past the buffer's end
+      if (p < a.M) {
+        const int n = p / (a.H * a.W), rem = p - n * a.H * a.W, h = rem / a.W, w = rem - h * a.W;
+        bq = (uint32_t)(((int64_t)((n * Hp + h) * Wp + w) * a.Ck + 8 * c) * 2);
+      }
+      base[q] = bq;
     }
     const uint32_t d0 = ldsa + (uint32_t)(FM * aw * 1024);
     auto issue = [&](int S) {
@@ -170,6 +191,10 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
       issue(S + CV_NA - 1);           // into the slot of S-1
     }
     vm_barrier<0>();
+  } else if (hc >= 0 && (wave >> 2) != hc) {
+    // ------------------------------- MMA waves of a half tile's other channels: the slab
+    // barriers B_0 .. B_nsl only
+    for (int S = 0; S <= nsl; ++S) lds_barrier();
   } else {
     // --------------------------------------------------------------- MMA group
     const int fi = lane & 15, kg = lane >> 4;
@@ -252,15 +277,16 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
         for (int e = 0; e < 4; ++e) stg[(16 * (mb0 + i) + 4 * kg + e) * CV_PITCH + 16 * (nb0 + j) + fi] = acc[i][j][e];
   }
   lds_barrier();
-  // ---- write the interior positions' rows
+  // ---- write the tile's rows (output position p is row p of the output); a half tile
+  // its 128 channels
   const float *stg = reinterpret_cast<const float *>(smem);
-  const int Hp = a.H + 2;
   if (a.out_bf16) {
-    const int ch = tid & 31, sub = tid >> 5;  // 8 channels per thread, NT/32 rows per pass
-    for (int m = sub; m < BM; m += NT / 32) {
-      const int P = m0 + m;
-      const int n = P / (Hp * Wp), rem = P - n * Hp * Wp, h = rem / Wp, w = rem - h * Wp;
-      if (P < a.M && h < a.H && w < a.W) {
+    // 8 channels per thread, 32 (16) threads per row
+    const int ch = hc < 0 ? (tid & 31) : 16 * hc + (tid & 15), sub = hc < 0 ? tid >> 5 : tid >> 4;
+    const int step = hc < 0 ? NT / 32 : NT / 16;
+    for (int m = sub; m < BM; m += step) {
+      const int p = m0 + m;
+      if (p < a.M) {
         const f32x4 v0 = *reinterpret_cast<const f32x4 *>(stg + m * CV_PITCH + 8 * ch);
         const f32x4 v1 = *reinterpret_cast<const f32x4 *>(stg + m * CV_PITCH + 8 * ch + 4);
         u32x4 pk;
@@ -268,18 +294,19 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
         pk[1] = cvt_pk_bf16(v0[2], v0[3]);
         pk[2] = cvt_pk_bf16(v1[0], v1[1]);
         pk[3] = cvt_pk_bf16(v1[2], v1[3]);
-        uint16_t *o = reinterpret_cast<uint16_t *>(a.out) + ((int64_t)(n * a.H + h) * a.W + w) * CV_BN + 8 * ch;
+        uint16_t *o = reinterpret_cast<uint16_t *>(a.out) + (int64_t)p * CV_BN + 8 * ch;
         *reinterpret_cast<u32x4 *>(o) = pk;
       }
     }
   } else {
-    const int ch = tid & 63, sub = tid >> 6;  // 4 channels per thread, NT/64 rows per pass
-    for (int m = sub; m < BM; m += NT / 64) {
-      const int P = m0 + m;
-      const int n = P / (Hp * Wp), rem = P - n * Hp * Wp, h = rem / Wp, w = rem - h * Wp;
-      if (P < a.M && h < a.H && w < a.W) {
+    // 4 channels per thread, 64 (32) threads per row
+    const int ch = hc < 0 ? (tid & 63) : 32 * hc + (tid & 31), sub = hc < 0 ? tid >> 6 : tid >> 5;
+    const int step = hc < 0 ? NT / 64 : NT / 32;
+    for (int m = sub; m < BM; m += step) {
+      const int p = m0 + m;
+      if (p < a.M) {
         const f32x4 v = *reinterpret_cast<const f32x4 *>(stg + m * CV_PITCH + 4 * ch);
-        float *o = reinterpret_cast<float *>(a.out) + ((int64_t)(n * a.H + h) * a.W + w) * CV_BN + 4 * ch;
+        float *o = reinterpret_cast<float *>(a.out) + (int64_t)p * CV_BN + 4 * ch;
         *reinterpret_cast<f32x4 *>(o) = v;
       }
     }
@@ -562,14 +589,20 @@ int run_conv_nt(int pass, int N, int H, int W, int Ci, int Co, const void *act, 
   a.w = reinterpret_cast<const uint16_t *>(w);
   a.out = out;
   a.out_bf16 = out_dtype == IMBD_BF16 ? 1 : 0;
+  a.N = N;
   a.H = H;
   a.W = W;
   a.Ck = pass == 1 ? Ci : Co;
   a.Cw = Ci;
-  // positions up to the last interior one of the padded grid
-  a.M = (int)((int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W);
+  a.M = N * H * W;
   a.tiles = (a.M + CV_BM - 1) / CV_BM;
-  const int grid = (a.tiles + 7) / 8 * 8;
+  // One workgroup per CU (160 KB of LDS): past one round, the tiles of a short last round
+  // run as 128-channel halves on twice as many CUs, which ends that round sooner.
+  const int last = a.tiles > CV_CUS ? a.tiles % CV_CUS : 0;
+  const bool halves = last > 0 && 2 * last <= CV_CUS;
+  a.tfull = halves ? a.tiles - last : a.tiles;
+  a.gfull = (a.tfull + 7) / 8 * 8;
+  const int grid = a.gfull + (halves ? 2 * last : 0);
   {
     LaunchTimer t(pass == 1 ? IMBD_K_CONV_FWD : IMBD_K_CONV_DGRAD, 0, s);
     if (pass == 1) hipLaunchKernelGGL(conv_nt_kernel<false>, dim3(grid), dim3(768), 0, s, a);

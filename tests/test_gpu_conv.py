@@ -136,6 +136,32 @@ def test_conv_tile_128_position_tiles_sampled(imbd, dev):
     assert torch.isfinite(y).all().item() and torch.isfinite(dx).all().item() and torch.isfinite(dw).all().item()
 
 
+@pytest.mark.parametrize("N,H,W", [(4, 92, 92), (4, 113, 113)])
+def test_conv_tile_last_round_sampled(imbd, dev, N, H, W):
+    """More 128-position tiles than one round of workgroups on 256 CUs: 4 x 92 x 92 has
+    265 tiles, whose last 9 run as 128-channel halves (18 workgroups); 4 x 113 x 113 has
+    400, whose last 144 run whole. Every channel of rows in the last round's tiles and
+    random outputs elsewhere, fp32 and bf16 outputs, forward and input gradient."""
+    _flush(f"conv last round {(N, H, W)}")
+    C = 256
+    d = make_conv_inputs(N, H, W, C, C, seed=H, border=(True, True, False, False))
+    xv, wv, dyv = bf16_values(d["x_bits"]), bf16_values(d["w_bits"]), bf16_values(d["dy_bits"])
+    M = N * H * W
+    rng = np.random.default_rng(H)
+    rows = np.array([256 * 128, 256 * 128 + 1, (M + 256 * 128) // 2, M - 129, M - 1])
+    full = (rows[:, None] * C + np.arange(C)[None, :]).reshape(-1)
+    idx = np.concatenate([full, rng.choice(M * C, 300, replace=False)])
+    ry = oracle.conv3x3_fwd_at(xv, wv, idx)
+    rx = oracle.conv3x3_dgrad_at(dyv, wv, idx)
+    for out_bf16 in (False, True):
+        y, dx, _ = _run(imbd, dev, d, out_bf16=out_bf16)
+        tol = 2.0 ** -8 + 1e-5 if out_bf16 else 1e-5
+        assert nrm_err(host(y).reshape(-1)[idx], ry) < tol
+        assert nrm_err(host(dx).reshape(-1)[idx], rx) < tol
+        import torch
+        assert torch.isfinite(y).all().item() and torch.isfinite(dx).all().item()
+
+
 def test_conv_stitched_domain_split(imbd, dev):
     """Domain parallelism on one GPU: a 2x2 split of a zero-padded image with exchanged
     halos (cut from the full padded tensor) reproduces the full-image conv, the summed
