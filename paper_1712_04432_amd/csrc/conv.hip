@@ -478,11 +478,30 @@ __global__ void __launch_bounds__(512, 1) conv_wg_kernel(CwArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) xd[j] = tr8(xs + fx[j] + (uint32_t)(s * 4096));
     };
-    auto mma = [&](const bf16x8 (&df)[FM], const bf16x8 (&xf)[4]) {
+    // One 32-k step: its 32 MFMAs in eight groups (row block g against the four column
+    // blocks), with the next step's twelve fragments (24 transpose reads) read two per group
+    // in the first six, the column blocks and the first row blocks first (the next step's
+    // first groups use them). Reading all 24 ahead of the MFMAs made every step wait for ten
+    // of them: the LDS counter tracks at most 15 operations, so the wait that the older
+    // fragments need also covers the oldest of the new reads. The last two groups' MFMAs
+    // cover the reads before the next step or the slab barrier.
+    auto step = [&](const bf16x8 (&df)[FM], const bf16x8 (&xf)[4], uint32_t dsn, uint32_t xsn, int sn,
+                    bf16x8 (&dd)[FM], bf16x8 (&xd)[4]) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int g = 0; g < FM; ++g) {
+        if (g < 6) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(df[i], xf[j], acc[i][j], 0, 0, 0);
+          for (int h = 0; h < 2; ++h) {
+            const int f = 2 * g + h;
+            if (f < 4) xd[f] = tr8(xsn + fx[f] + (uint32_t)(sn * 4096));
+            else dd[f - 4] = tr8(dsn + fa[f - 4] + (uint32_t)(sn * 4096));
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(df[g], xf[j], acc[g][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     };
     uint32_t ds = ldsd, xs = ldsx;
     if (nsl > 0) {
@@ -490,17 +509,11 @@ __global__ void __launch_bounds__(512, 1) conv_wg_kernel(CwArgs a) {
       read(ds, xs, 0, dv[0], xv[0]);
     }
     for (int S = 0; S < nsl; ++S) {
-      read(ds, xs, 1, dv[1], xv[1]);
-      __builtin_amdgcn_sched_barrier(0);
-      mma(dv[0], xv[0]);
-      __builtin_amdgcn_sched_barrier(0);
+      step(dv[0], xv[0], ds, xs, 1, dv[1], xv[1]);
       lds_barrier();  // B_{S+1}
       ds = ldsd + (uint32_t)(((S + 1) % CW_ND) * CW_DSLOT);
       xs = ldsx + (uint32_t)(((S + 1) % CW_NX) * CW_XSLOT);
-      read(ds, xs, 0, dv[0], xv[0]);  // past the last slab this reads a spent slot, unused
-      __builtin_amdgcn_sched_barrier(0);
-      mma(dv[1], xv[1]);
-      __builtin_amdgcn_sched_barrier(0);
+      step(dv[1], xv[1], ds, xs, 0, dv[0], xv[0]);  // past the last slab this reads a spent slot, unused
     }
     if (nsl == 0) lds_barrier();  // the loaders' B_0 (they pass vm_barrier<0> once)
     // ---- stage the tile as [output channel][input channel] fp32
