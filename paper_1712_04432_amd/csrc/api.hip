@@ -467,8 +467,10 @@ static GemmProblem local_dx_problem(int dtype, int d_out_blk, int d_in, int b_bl
 
 // A bf16 Delta_Y block whose rows are not whole 16-byte chunks (a 250-row block of the
 // 1000-wide top layer has a 500-byte pitch; any block of a width that is not a multiple
-// of 8) is copied once into the workspace with its rows padded with zeros to a multiple
-// of 8 elements, so that both backward products run on the large-tile kernels.
+// of 8): where its rows are 4-byte aligned and the paired launch takes both backward
+// products, both read it in place in 4-byte pieces; otherwise it is copied once into the
+// workspace with its rows padded with zeros to a multiple of 8 elements, so that both
+// products run on the large-tile kernels.
 static size_t local_dy_copy_bytes(int dtype, int d_out_blk, int b_blk) {
   if (dtype != IMBD_BF16 || b_blk <= 0) return 0;
   return align256((size_t)b_blk * (size_t)((d_out_blk + 7) / 8 * 8) * 2);
@@ -514,6 +516,50 @@ int mlp_local_fwd(int dtype, int relu, int P_r, int P_c, int d_out_blk, int d_in
   return gemm_run(p, ws, ws_bytes, reinterpret_cast<hipStream_t>(stream));
 }
 
+// The local backward pass's two products: the Delta_W (+ bias) partial and the Delta_X
+// partial, on the block's operands as given.
+static GemmProblem local_dw_bwd_problem(int dtype, int d_out_blk, int d_in, int b_blk, const void *x_blk, int64_t ldx,
+                                        const void *dy_blk, int64_t lddy, float *dw_part, int64_t lddw,
+                                        float *db_part, float scale) {
+  GemmProblem pw = local_dw_problem(dtype, d_out_blk, d_in, b_blk);
+  pw.A = x_blk;
+  pw.lda = ldx;
+  pw.B = dy_blk;
+  pw.ldb = lddy;
+  if (db_part) {
+    pw.db_mode = 1;
+    pw.db_out = db_part;
+    pw.db_alpha = scale;
+  }
+  pw.epi.mode = EPI_STORE;
+  pw.epi.alpha = scale;
+  pw.epi.out = dw_part;
+  pw.epi.ldo = lddw;
+  pw.epi.out_dtype = IMBD_F32;
+  return pw;
+}
+
+static GemmProblem local_dx_bwd_problem(int dtype, int d_out_blk, int d_in, int b_blk, const void *w_blk, int64_t ldw,
+                                        const void *dy_blk, int64_t lddy, const void *x_blk, int64_t ldx,
+                                        float *dx_part, int64_t lddx, int mask_relu, bool kpad8) {
+  GemmProblem p = local_dx_problem(dtype, d_out_blk, d_in, b_blk);
+  p.b_kpad8 = kpad8;
+  p.A = w_blk;
+  p.lda = ldw;
+  p.B = dy_blk;
+  p.ldb = lddy;
+  p.epi.mode = EPI_STORE;
+  if (mask_relu) {
+    p.epi.mask = x_blk;
+    p.epi.ldmask = ldx;
+    p.epi.mask_dtype = dtype;
+  }
+  p.epi.out = dx_part;
+  p.epi.ldo = lddx;
+  p.epi.out_dtype = IMBD_F32;
+  return p;
+}
+
 int mlp_local_bwd(int dtype, int P_r, int P_c, int d_out_blk, int d_in, int b_blk, const void *w_blk, int64_t ldw,
                   const void *dy_blk, int64_t lddy, const void *x_blk, int64_t ldx, float *dw_part, int64_t lddw,
                   float *db_part, float *dx_part, int64_t lddx, int mask_relu, void *ws, size_t ws_bytes,
@@ -533,7 +579,18 @@ int mlp_local_bwd(int dtype, int P_r, int P_c, int d_out_blk, int d_in, int b_bl
   // sums after it
   const size_t cpy = local_dy_copy_bytes(dtype, d_out_blk, b_blk);
   bool copied = false;
-  if (b_blk > 0 && local_dy_needs_copy(dtype, d_out_blk, dy_blk, lddy)) {
+  const bool needs_copy = b_blk > 0 && local_dy_needs_copy(dtype, d_out_blk, dy_blk, lddy);
+  if (needs_copy && dx_part) {
+    // rows of Delta_Y 4-byte aligned: the paired launch may read them in place
+    GemmProblem pw = local_dw_bwd_problem(dtype, d_out_blk, d_in, b_blk, x_blk, ldx, dy_blk, lddy, dw_part, lddw,
+                                          db_part, scale);
+    GemmProblem p = local_dx_bwd_problem(dtype, d_out_blk, d_in, b_blk, w_blk, ldw, dy_blk, lddy, x_blk, ldx,
+                                         dx_part, lddx, mask_relu, false);
+    void *wsp = ws && cpy > 0 ? reinterpret_cast<char *>(ws) + cpy : ws;
+    const int rc = run_local_dx_dw_pair(p, pw, wsp, s, true);
+    if (rc != 1) return rc;
+  }
+  if (needs_copy) {
     if (!ws || (uintptr_t)ws % 256 != 0 || ws_bytes < cpy)
       FAIL(IMBD_EWORKSPACE, "the Delta_Y block needs an aligned copy: workspace of %zu bytes, 256-byte aligned, "
                             "need at least %zu", ws_bytes, cpy);
@@ -548,40 +605,14 @@ int mlp_local_bwd(int dtype, int P_r, int P_c, int d_out_blk, int d_in, int b_bl
     ws = ws ? reinterpret_cast<char *>(ws) + cpy : nullptr;
     ws_bytes = ws_bytes > cpy ? ws_bytes - cpy : 0;
   }
-  GemmProblem pw = local_dw_problem(dtype, d_out_blk, d_in, b_blk);
-  pw.A = x_blk;
-  pw.lda = ldx;
-  pw.B = dy_blk;
-  pw.ldb = lddy;
-  if (db_part) {
-    pw.db_mode = 1;
-    pw.db_out = db_part;
-    pw.db_alpha = scale;
-  }
-  pw.epi.mode = EPI_STORE;
-  pw.epi.alpha = scale;
-  pw.epi.out = dw_part;
-  pw.epi.ldo = lddw;
-  pw.epi.out_dtype = IMBD_F32;
+  const GemmProblem pw = local_dw_bwd_problem(dtype, d_out_blk, d_in, b_blk, x_blk, ldx, dy_blk, lddy, dw_part, lddw,
+                                              db_part, scale);
   if (dx_part && b_blk > 0) {
-    GemmProblem p = local_dx_problem(dtype, d_out_blk, d_in, b_blk);
-    p.b_kpad8 = copied;
-    p.A = w_blk;
-    p.lda = ldw;
-    p.B = dy_blk;
-    p.ldb = lddy;
-    p.epi.mode = EPI_STORE;
-    if (mask_relu) {
-      p.epi.mask = x_blk;
-      p.epi.ldmask = ldx;
-      p.epi.mask_dtype = dtype;
-    }
-    p.epi.out = dx_part;
-    p.epi.ldo = lddx;
-    p.epi.out_dtype = IMBD_F32;
+    const GemmProblem p = local_dx_bwd_problem(dtype, d_out_blk, d_in, b_blk, w_blk, ldw, dy_blk, lddy, x_blk, ldx,
+                                               dx_part, lddx, mask_relu, copied);
     // the two products are independent: one launch when both run on the large-tile
     // kernels without partial sums
-    const int rc = run_local_dx_dw_pair(p, pw, ws, s);
+    const int rc = run_local_dx_dw_pair(p, pw, ws, s, false);
     if (rc != 1) return rc;
     TRY(gemm_run(p, ws, ws_bytes, s));
   }

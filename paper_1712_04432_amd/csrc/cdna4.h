@@ -38,6 +38,15 @@ __device__ __forceinline__ void dma16(const i32x4 &rsrc, uint32_t voff, uint32_t
                : "memory");
 }
 
+// The 4-byte form: 64 x 4 bytes to LDS at lds_base + 4*lane (for rows whose pitch is a
+// multiple of 4 bytes only; four of these stand in for one 16-byte load).
+__device__ __forceinline__ void dma4(const i32x4 &rsrc, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_nop 0\n\tbuffer_load_dword %0, %1, 0 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "{m0}"(lds_base)
+               : "memory");
+}
+
 template <int VM>
 __device__ __forceinline__ void vm_barrier() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(VM) : "memory");

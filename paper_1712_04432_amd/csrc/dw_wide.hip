@@ -75,6 +75,7 @@ void dw_wide_prepare(const GemmProblem &p, int extra_blocks, DlArgs *out, int *o
   // and a chunk that crossed a tighter end would read as zero whole (columns of the last
   // sample dropped); columns past N only feed outputs that are not stored
   a.dy_bytes = (uint32_t)(((int64_t)(p.K - 1) * p.ldb + (p.N + 7) / 8 * 8) * 2);
+  a.dy_dw4 = 0;
   a.M = p.M;
   a.N = p.N;
   a.K = p.K;

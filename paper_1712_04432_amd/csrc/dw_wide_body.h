@@ -34,6 +34,8 @@ struct DlArgs {
   int db_mode;
   float db_alpha, bias_lr;
   float *db_out, *bias;
+  // Delta_Y's rows only 4-byte aligned (pitch and base): loaded in 4-byte pieces
+  int dy_dw4;
 };
 
 __device__ __forceinline__ int dl_swz(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
@@ -114,26 +116,64 @@ __device__ __forceinline__ void dw_wide_body(const DlArgs &a, char *smem, int bi
     constexpr int QN = QB * NQ / 2;  // 1 KB blocks per wave
     const int dw = wave - 6;
     const i32x4 rd = buf_rsrc(a.DY, a.dy_bytes);
-    uint32_t base[QN], dst[QN];
-#pragma unroll
-    for (int q = 0; q < QN; ++q) {
-      const int h = (NQ / 2) * dw + q / QB, g = q % QB;
-      const int r = 8 * g + (lane >> 3);
-      const int c = (lane & 7) ^ dl_swz(r);
-      base[q] = (uint32_t)(((int64_t)r * a.lddy + o0 + 64 * h + 8 * c) * 2);
-      dst[q] = (uint32_t)(h * QSLOT + g * 1024);
-    }
     const uint32_t sstep = (uint32_t)(SK * a.lddy * 2);
-    auto issue = [&](int S) {
-      const uint32_t slot = ldsd + (uint32_t)((S % ND) * DSLOT);
+    // Rows 4-byte aligned only: each 16-byte chunk of the layout below comes as four 4-byte
+    // loads. Instruction i of a 1 KB block fills its bytes 256i .. 256i + 255: lane l loads
+    // dword l%4 of the chunk that lane 16i + l/4 loads in the 16-byte form. Columns past N
+    // feed only outputs that are not stored; the descriptor ends at the last sample's
+    // column N (N even).
+    constexpr bool DW4_OK = 4 * QN * (ND - 2) <= 63;  // the memory counter's range
+    if (DW4_OK && a.dy_dw4) {
+      uint32_t b4[QN][4];
 #pragma unroll
-      for (int q = 0; q < QN; ++q) dma16(rd, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
-    };
+      for (int q = 0; q < QN; ++q) {
+        const int h = (NQ / 2) * dw + q / QB, g = q % QB;
 #pragma unroll
-    for (int S = 0; S < ND - 1; ++S) issue(S);
-    for (int S = 0; S < nsl; ++S) {
-      vm_barrier<QN * (ND - 2)>();  // slab S landed: B_S
-      issue(S + ND - 1);            // into the slot of S-1
+        for (int i = 0; i < 4; ++i) {
+          const int L = 16 * i + (lane >> 2);
+          const int r = 8 * g + (L >> 3);
+          const int c = (L & 7) ^ dl_swz(r);
+          b4[q][i] = (uint32_t)(((int64_t)r * a.lddy + o0 + 64 * h + 8 * c) * 2 + 4 * (lane & 3));
+        }
+      }
+      auto issue4 = [&](int S) {
+        const uint32_t slot = ldsd + (uint32_t)((S % ND) * DSLOT);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) {
+          const int h = (NQ / 2) * dw + q / QB, g = q % QB;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            dma4(rd, S < nsl ? b4[q][i] + (uint32_t)S * sstep : OOB,
+                 slot + (uint32_t)(h * QSLOT + g * 1024 + 256 * i));
+        }
+      };
+#pragma unroll
+      for (int S = 0; S < ND - 1; ++S) issue4(S);
+      for (int S = 0; S < nsl; ++S) {
+        vm_barrier<(DW4_OK ? 4 : 1) * QN * (ND - 2)>();  // slab S landed: B_S
+        issue4(S + ND - 1);                              // into the slot of S-1
+      }
+    } else {
+      uint32_t base[QN], dst[QN];
+#pragma unroll
+      for (int q = 0; q < QN; ++q) {
+        const int h = (NQ / 2) * dw + q / QB, g = q % QB;
+        const int r = 8 * g + (lane >> 3);
+        const int c = (lane & 7) ^ dl_swz(r);
+        base[q] = (uint32_t)(((int64_t)r * a.lddy + o0 + 64 * h + 8 * c) * 2);
+        dst[q] = (uint32_t)(h * QSLOT + g * 1024);
+      }
+      auto issue = [&](int S) {
+        const uint32_t slot = ldsd + (uint32_t)((S % ND) * DSLOT);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) dma16(rd, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
+      };
+#pragma unroll
+      for (int S = 0; S < ND - 1; ++S) issue(S);
+      for (int S = 0; S < nsl; ++S) {
+        vm_barrier<QN * (ND - 2)>();  // slab S landed: B_S
+        issue(S + ND - 1);            // into the slot of S-1
+      }
     }
     vm_barrier<0>();
     if constexpr (EARLY) load_masters();

@@ -54,6 +54,8 @@ struct SkArgs {
   float *aux_loss;
   int aux_n;
   float aux_scale;
+  // B's rows only 4-byte aligned (pitch and base): loaded in 4-byte pieces (NB <= 2), K even
+  int b_dw4;
 };
 
 // Partial-sum layout: each workgroup's 64 x N tile is one contiguous block (a tile pitch
@@ -117,32 +119,70 @@ __device__ __forceinline__ void skinny_body(const SkArgs &a, char *smem, int bid
     // blocks 4NB*xw .. 4NB*xw + 4NB-1 of the slot (8 rows x 128 B each).
     const int xw = wave - 6;
     const i32x4 rb = buf_rsrc(a.B, (uint32_t)((int64_t)a.N * a.ldb * 2));
-    uint32_t base[4 * NB];
-    int kof[4 * NB];
-#pragma unroll
-    for (int q = 0; q < 4 * NB; ++q) {
-      const int r = 8 * (4 * NB * xw + q) + (lane >> 3);
-      const int c = (lane & 7) ^ swz_kc(r);
-      base[q] = (uint32_t)(((int64_t)(n0 + r) * a.ldb + klo + 8 * c) * 2);  // rows past N: out of range
-      kof[q] = 8 * c;
-    }
     const uint32_t dst0 = ldsx + (uint32_t)(4 * NB * xw * 1024);
     uint32_t slot = 0;  // ring slot of the next slab to issue
-    auto issue = [&](int S) {
+    // B's rows 4-byte aligned only (NB <= 2): each 16-byte chunk of the layout below comes
+    // as four 4-byte loads. Instruction i of a 1 KB block fills its bytes 256i .. 256i + 255:
+    // lane l loads dword l%4 of the chunk that lane 16i + l/4 loads in the 16-byte form
+    // (rows of block q are those of block 0 plus 8q, with the same swizzle). A dword past
+    // the K-range (K even) reads as zero.
+    constexpr bool DW4_OK = 4 * 4 * NB * (SK_NX - 2) <= 63;  // the memory counter's range
+    if (DW4_OK && a.b_dw4) {
+      uint32_t b4[4];
+      int k4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int L = 16 * i + (lane >> 2), d = lane & 3;
+        const int r = 8 * (4 * NB * xw) + (L >> 3);
+        const int c = (L & 7) ^ swz_kc(r);
+        b4[i] = (uint32_t)(((int64_t)(n0 + r) * a.ldb + klo + 8 * c) * 2 + 4 * d);
+        k4[i] = 8 * c + 2 * d;
+      }
+      const uint32_t qstep = (uint32_t)(8 * a.ldb * 2);
+      auto issue4 = [&](int S) {
+#pragma unroll
+        for (int q = 0; q < 4 * NB; ++q)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const bool ok = S * SK_KS + k4[i] < krange;
+            dma4(rb, ok ? b4[i] + (uint32_t)q * qstep + (uint32_t)S * 128u : OOB,
+                 dst0 + slot + (uint32_t)(q * 1024 + 256 * i));
+          }
+        slot = slot + XSLOT == XRING ? 0u : slot + XSLOT;
+      };
+#pragma unroll
+      for (int S = 0; S < SK_NX - 1; ++S) issue4(S);
+      for (int S = 0; S < nsl; ++S) {
+        vm_barrier<(DW4_OK ? 4 : 1) * 4 * NB * (SK_NX - 2)>();  // slab S landed: B_S
+        issue4(S + SK_NX - 1);                                 // into the slot of S-1
+      }
+      vm_barrier<0>();
+    } else {
+      uint32_t base[4 * NB];
+      int kof[4 * NB];
 #pragma unroll
       for (int q = 0; q < 4 * NB; ++q) {
-        const bool ok = S * SK_KS + kof[q] < krange;
-        dma16(rb, ok ? base[q] + (uint32_t)S * 128u : OOB, dst0 + slot + q * 1024);
+        const int r = 8 * (4 * NB * xw + q) + (lane >> 3);
+        const int c = (lane & 7) ^ swz_kc(r);
+        base[q] = (uint32_t)(((int64_t)(n0 + r) * a.ldb + klo + 8 * c) * 2);  // rows past N: out of range
+        kof[q] = 8 * c;
       }
-      slot = slot + XSLOT == XRING ? 0u : slot + XSLOT;
-    };
+      auto issue = [&](int S) {
 #pragma unroll
-    for (int S = 0; S < SK_NX - 1; ++S) issue(S);
-    for (int S = 0; S < nsl; ++S) {
-      vm_barrier<4 * NB * (SK_NX - 2)>();  // slab S landed: B_S
-      issue(S + SK_NX - 1);                // into the slot of S-1
+        for (int q = 0; q < 4 * NB; ++q) {
+          const bool ok = S * SK_KS + kof[q] < krange;
+          dma16(rb, ok ? base[q] + (uint32_t)S * 128u : OOB, dst0 + slot + q * 1024);
+        }
+        slot = slot + XSLOT == XRING ? 0u : slot + XSLOT;
+      };
+#pragma unroll
+      for (int S = 0; S < SK_NX - 1; ++S) issue(S);
+      for (int S = 0; S < nsl; ++S) {
+        vm_barrier<4 * NB * (SK_NX - 2)>();  // slab S landed: B_S
+        issue(S + SK_NX - 1);                // into the slot of S-1
+      }
+      vm_barrier<0>();
     }
-    vm_barrier<0>();
   } else if (wave >= 4) {
     // ------------------------------------------------------------ W loaders (4, 5)
     // KC slab: W rows m0..m0+63 x k = klo + 64S ..; TR slab: k-rows klo + 64S .. x
@@ -810,13 +850,28 @@ size_t skinny_ws_bytes(const GemmProblem &p) {
   return (size_t)pl.splits * (size_t)sk_split_pitch(p.M, p.N) * sizeof(float);
 }
 
-int run_local_dx_dw_pair(const GemmProblem &dx, const GemmProblem &dw, void *ws, hipStream_t s) {
+int run_local_dx_dw_pair(const GemmProblem &dx, const GemmProblem &dw, void *ws, hipStream_t s, bool dy_dw4) {
   constexpr int NOT_TAKEN = 1;
   if (opt(IMBD_OPT_LOCAL_PAIR) == 0 || opt(IMBD_OPT_SKINNY_OFF) != 0) return NOT_TAKEN;
   if (dx.M <= 0 || dx.N <= 0 || dw.M <= 0 || dw.N <= 0 || dx.aux_loss || !dx.b_kc || dx.a_kc) return NOT_TAKEN;
-  if (!skinny_fits(dx) || !sk_fused_ok(dx) || !dw_wide_fits(dw) || dw.epi.mode != EPI_STORE) return NOT_TAKEN;
+  if (dy_dw4) {
+    // Delta_Y in 4-byte pieces: its rows 4-byte aligned, an even K for the Delta_X product
+    // (so that a piece never straddles K) and an even width for the Delta_W product's
+    // descriptor end; the other conditions are checked on stand-ins with 16-byte rows
+    if (dx.B != dw.B || dx.ldb != dw.ldb || (reinterpret_cast<uintptr_t>(dx.B) % 4) != 0 || dx.ldb % 2 != 0 ||
+        dx.K % 2 != 0 || dw.N % 2 != 0 || dx.N > 128)
+      return NOT_TAKEN;
+    GemmProblem sx = dx, sw = dw;
+    sx.B = sw.B = reinterpret_cast<const void *>((uintptr_t)256);
+    sx.ldb = sw.ldb = (dx.ldb + 7) / 8 * 8;
+    sx.b_kpad8 = true;
+    if (!skinny_fits(sx) || !sk_fused_ok(dx) || !dw_wide_fits(sw) || dw.epi.mode != EPI_STORE) return NOT_TAKEN;
+  } else if (!skinny_fits(dx) || !sk_fused_ok(dx) || !dw_wide_fits(dw) || dw.epi.mode != EPI_STORE) {
+    return NOT_TAKEN;
+  }
   const SkPlan pl = sk_plan(dx);
   if (pl.splits != 1) return NOT_TAKEN;  // its reduce would follow the pair
+  if (dy_dw4 && pl.nb > 2) return NOT_TAKEN;
   // the large-tile product alone on two workgroups per CU (a launch of its own is faster)
   // or with its bias on the column-sum kernel: not paired
   DlArgs d;
@@ -828,6 +883,12 @@ int run_local_dx_dw_pair(const GemmProblem &dx, const GemmProblem &dw, void *ws,
   const int n_sk = prepare_skinny(dx, pl, ws, true, &g);
   const int n_pad = (n_sk + 7) / 8 * 8;
   dw_wide_prepare(dw, n_pad, &d, &oh, &dual, &g_dl);
+  if (dy_dw4) {
+    if (oh != 128) return NOT_TAKEN;  // 256-row tiles: more pieces in flight than the counter holds
+    g.b_dw4 = 1;
+    d.dy_dw4 = 1;
+    d.dy_bytes = (uint32_t)(((int64_t)(dw.K - 1) * dw.ldb + dw.N) * 2);
+  }
   const int grid = n_pad + g_dl;
   {
     LaunchTimer t(dw.kclass, dw.layer, s);

@@ -256,6 +256,41 @@ def test_local_bwd_one_launch_matches_two(imbd, dev, shape):
     assert nrm_err(out[1][0], rdw) < 1e-5 and nrm_err(out[1][1], rdb) < 1e-5 and nrm_err(out[1][2], rdx) < 1e-5
 
 
+@pytest.mark.parametrize("col0", [250, 2])
+def test_local_bwd_dy_block_of_wider_rows(imbd, dev, col0):
+    """The Delta_Y block as a view of the full top-layer gradient (64 x 1000, 2000-byte
+    rows): a process's 250 columns from col0 on, rows 4-byte aligned but not 16-byte
+    aligned. The paired launch reads them in place in 4-byte pieces; every bit equals the
+    two-launch route (which copies the block into aligned rows) and the oracle agrees."""
+    import torch
+    _flush(f"local_bwd Delta_Y view at column {col0}")
+    dout, din, b = 250, 1024, 64
+    d, W, X, _ = _local_inputs(dout, din, b, "bf16", seed=7)
+    rng = np.random.default_rng(col0)
+    full = to_bf16_bits(rng.standard_normal((b, 1000)).astype(np.float32))
+    DY = bf16_values(full)[:, col0:col0 + dout]
+    wd, xd = _to_dev(d, "w", "bf16", dev), _to_dev(d, "x", "bf16", dev)
+    dyd = dev_bf16_bits(full, dev)[:, col0:col0 + dout]
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(1, imbd.IMBD_BF16, dout, din, b), 16),
+                     dtype=torch.uint8, device=dev)
+    out = {}
+    for pair in (1, 0):
+        dw = torch.full((dout, din), 7.0, device=dev)
+        db = torch.full((dout,), 7.0, device=dev)
+        dx = torch.full((b, din), 7.0, device=dev)
+        with imbd.options(local_pair=pair):
+            imbd.timing_begin(imbd.IMBD_K_GEMM_DX, -1, 16)
+            imbd.mlp_local_bwd(wd, dyd, xd, dw, 4, 16, db_part=db, dx_part=dx, mask_relu=True, ws=ws)
+            n_dx, _ = imbd.timing_end()
+        torch.cuda.synchronize()
+        out[pair] = (host(dw), host(db), host(dx), n_dx)
+    assert out[1][3] == 0 and out[0][3] == 1, (out[1][3], out[0][3])
+    for a, c in zip(out[1][:3], out[0][:3]):
+        assert np.array_equal(a, c)
+    rdw, rdb, rdx = oracle.local_bwd(W, DY, X, 1.0 / (b * 16), mask_src=X)
+    assert nrm_err(out[1][0], rdw) < 1e-5 and nrm_err(out[1][1], rdb) < 1e-5 and nrm_err(out[1][2], rdx) < 1e-5
+
+
 def test_local_fwd_strided_views(imbd, dev):
     """Blocks passed as views of a larger array (leading dimension > row length)."""
     import torch
