@@ -586,8 +586,9 @@ int mlp_local_bwd(int dtype, int P_r, int P_c, int d_out_blk, int d_in, int b_bl
                                           db_part, scale);
     GemmProblem p = local_dx_bwd_problem(dtype, d_out_blk, d_in, b_blk, w_blk, ldw, dy_blk, lddy, x_blk, ldx,
                                          dx_part, lddx, mask_relu, false);
+    p.b_dw4 = pw.b_dw4 = true;
     void *wsp = ws && cpy > 0 ? reinterpret_cast<char *>(ws) + cpy : ws;
-    const int rc = run_local_dx_dw_pair(p, pw, wsp, s, true);
+    const int rc = run_local_dx_dw_pair(p, pw, wsp, s);
     if (rc != 1) return rc;
   }
   if (needs_copy) {
@@ -612,7 +613,7 @@ int mlp_local_bwd(int dtype, int P_r, int P_c, int d_out_blk, int d_in, int b_bl
                                                dx_part, lddx, mask_relu, copied);
     // the two products are independent: one launch when both run on the large-tile
     // kernels without partial sums
-    const int rc = run_local_dx_dw_pair(p, pw, ws, s, false);
+    const int rc = run_local_dx_dw_pair(p, pw, ws, s);
     if (rc != 1) return rc;
     TRY(gemm_run(p, ws, ws_bytes, s));
   }

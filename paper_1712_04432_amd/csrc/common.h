@@ -87,6 +87,10 @@ struct GemmProblem {
   // B's rows hold zeros from K up to K rounded up to 8 (a copied block): the B <= 256
   // kernel may then take a K that is not a multiple of 8 when A is read by k-rows
   bool b_kpad8 = false;
+  // B's rows only 4-byte aligned (base and pitch): the B <= 128 product kernel and the
+  // 128-row large-tile weight-gradient kernel read them in 4-byte pieces (K even for the
+  // former, N even for the latter); other routes do not take such a problem
+  bool b_dw4 = false;
 };
 
 // Launch plan chosen for a product (a pure function of the shapes).

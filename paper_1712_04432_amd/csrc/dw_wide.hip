@@ -51,7 +51,8 @@ bool dw_wide_fits(const GemmProblem &p) {
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const int64_t lim = (int64_t)1 << 31;  // bytes in one buffer descriptor
   if (p.dtype != IMBD_BF16 || p.a_kc || p.b_kc || e.mask || e.bias || e.relu || p.K < min_k || p.K <= 0 ||
-      p.M <= 0 || p.N <= 0 || p.M % 8 || !al(p.A, 16) || !al(p.B, 16) || p.lda % 8 || p.ldb % 8 ||
+      p.M <= 0 || p.N <= 0 || p.M % 8 || !al(p.A, 16) || p.lda % 8 ||
+      (p.b_dw4 ? !al(p.B, 4) || p.ldb % 2 || p.N % 2 : !al(p.B, 16) || p.ldb % 8) ||
       p.lda < p.M || p.ldb < p.N || !al(e.out, 16) || e.ldo % 4 || e.ldo < p.M)
     return false;
   if (((int64_t)(p.K - 1) * p.lda + p.M) * 2 >= lim || ((int64_t)(p.K - 1) * p.ldb + (p.N + 7) / 8 * 8) * 2 >= lim ||
@@ -75,7 +76,9 @@ void dw_wide_prepare(const GemmProblem &p, int extra_blocks, DlArgs *out, int *o
   // and a chunk that crossed a tighter end would read as zero whole (columns of the last
   // sample dropped); columns past N only feed outputs that are not stored
   a.dy_bytes = (uint32_t)(((int64_t)(p.K - 1) * p.ldb + (p.N + 7) / 8 * 8) * 2);
-  a.dy_dw4 = 0;
+  // rows read in 4-byte pieces: the descriptor ends at the last sample's column N (even)
+  a.dy_dw4 = p.b_dw4 ? 1 : 0;
+  if (p.b_dw4) a.dy_bytes = (uint32_t)(((int64_t)(p.K - 1) * p.ldb + p.N) * 2);
   a.M = p.M;
   a.N = p.N;
   a.K = p.K;
@@ -99,7 +102,8 @@ void dw_wide_prepare(const GemmProblem &p, int extra_blocks, DlArgs *out, int *o
   // its launch only)
   const int dual_opt = opt(IMBD_OPT_DW_WIDE_DUAL);
   const bool dual = extra_blocks == 0 && (dual_opt == 1 || (dual_opt == -1 && t128 > 256));
-  const bool half = dual || ((t128 + 255) / 256) * 128 * 11 < ((t256 + 255) / 256) * 256 * 10;
+  // (4-byte pieces: 128-row tiles, whose loads in flight fit the memory counter)
+  const bool half = dual || p.b_dw4 || ((t128 + 255) / 256) * 128 * 11 < ((t256 + 255) / 256) * 256 * 10;
   const int oh = half ? 128 : 256;
   a.tiles_o = (p.N + oh - 1) / oh;
   a.tiles_i = (p.M + 127) / 128;

@@ -632,14 +632,18 @@ int nb_for(int N) { return N <= 64 ? 1 : N <= 128 ? 2 : 4; }
 bool skinny_dims_fit(const GemmProblem &p) {
   // K a multiple of 8 (whole 16-byte chunks), or B's rows zero-padded past K with A read by
   // k-rows (rows past K read as zero)
+  // (or B read in 4-byte pieces with K even: pieces past K read as zero)
   return p.dtype == IMBD_BF16 && p.b_kc && p.epi.mode == EPI_STORE && p.db_mode == 0 && p.N >= 1 &&
-         p.N <= 256 && p.M >= 1 && p.K >= 1 && (p.K % 8 == 0 || (p.b_kpad8 && !p.a_kc)) && (p.a_kc || p.M % 8 == 0);
+         p.N <= (p.b_dw4 ? 128 : 256) && p.M >= 1 && p.K >= 1 &&
+         (p.K % 8 == 0 || (p.b_kpad8 && !p.a_kc) || (p.b_dw4 && !p.a_kc && p.K % 2 == 0)) &&
+         (p.a_kc || p.M % 8 == 0);
 }
 
 bool skinny_fits(const GemmProblem &p) {
   auto al = [](const void *q, int a) { return (reinterpret_cast<uintptr_t>(q) % a) == 0; };
   const int64_t arows = p.a_kc ? p.M : p.K;
-  return skinny_dims_fit(p) && p.lda % 8 == 0 && p.ldb % 8 == 0 && al(p.A, 16) && al(p.B, 16) &&
+  const bool bal = p.b_dw4 ? p.ldb % 2 == 0 && al(p.B, 4) : p.ldb % 8 == 0 && al(p.B, 16);
+  return skinny_dims_fit(p) && p.lda % 8 == 0 && bal && al(p.A, 16) &&
          (arows + SK_KS + SK_BM) * p.lda * 2 < ((int64_t)1 << 31) &&
          ((int64_t)256 * p.ldb + p.K + SK_KS) * 2 < ((int64_t)1 << 31);
 }
@@ -671,10 +675,11 @@ static SkPlan sk_plan(const GemmProblem &p) {
   const double fix_part[5] = {0, 7100.0, 7100.0, 0, 13700.0};
   const int forced_s = opt(IMBD_OPT_SKINNY_SPLITS), forced_nb = opt(IMBD_OPT_SKINNY_NB);
   const bool fusable = sk_fused_ok(p);
-  SkPlan best{4, 1, 1, p.K};
+  SkPlan best{p.b_dw4 ? 2 : 4, 1, 1, p.K};
   double best_t = 1e30;
   for (int nb = 1; nb <= 4; nb *= 2) {
     if (forced_nb > 0 ? nb != forced_nb : nb > nb_for(p.N)) continue;
+    if (p.b_dw4 && nb > 2) continue;  // 4-byte pieces: at most 128 samples per workgroup
     const int tiles_n = (p.N + 64 * nb - 1) / (64 * nb);
     for (int s = 1; s <= 64; ++s) {
       const int ks = ((p.K + s - 1) / s + SK_KS - 1) / SK_KS * SK_KS;
@@ -727,6 +732,7 @@ static int prepare_skinny(const GemmProblem &p, const SkPlan &pl, void *ws, bool
   g.tpitch = sk_tile_pitch(p.N);
   g.sstride = sk_split_pitch(p.M, p.N);
   const Epilogue &e = p.epi;
+  g.b_dw4 = p.b_dw4 ? 1 : 0;
   g.fused = allow_fused && pl.splits == 1 && sk_fused_ok(p);
   if (g.fused) {
     auto al = [](const void *q, int a) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % a) == 0; };
@@ -850,28 +856,15 @@ size_t skinny_ws_bytes(const GemmProblem &p) {
   return (size_t)pl.splits * (size_t)sk_split_pitch(p.M, p.N) * sizeof(float);
 }
 
-int run_local_dx_dw_pair(const GemmProblem &dx, const GemmProblem &dw, void *ws, hipStream_t s, bool dy_dw4) {
+int run_local_dx_dw_pair(const GemmProblem &dx, const GemmProblem &dw, void *ws, hipStream_t s) {
   constexpr int NOT_TAKEN = 1;
   if (opt(IMBD_OPT_LOCAL_PAIR) == 0 || opt(IMBD_OPT_SKINNY_OFF) != 0) return NOT_TAKEN;
   if (dx.M <= 0 || dx.N <= 0 || dw.M <= 0 || dw.N <= 0 || dx.aux_loss || !dx.b_kc || dx.a_kc) return NOT_TAKEN;
-  if (dy_dw4) {
-    // Delta_Y in 4-byte pieces: its rows 4-byte aligned, an even K for the Delta_X product
-    // (so that a piece never straddles K) and an even width for the Delta_W product's
-    // descriptor end; the other conditions are checked on stand-ins with 16-byte rows
-    if (dx.B != dw.B || dx.ldb != dw.ldb || (reinterpret_cast<uintptr_t>(dx.B) % 4) != 0 || dx.ldb % 2 != 0 ||
-        dx.K % 2 != 0 || dw.N % 2 != 0 || dx.N > 128)
-      return NOT_TAKEN;
-    GemmProblem sx = dx, sw = dw;
-    sx.B = sw.B = reinterpret_cast<const void *>((uintptr_t)256);
-    sx.ldb = sw.ldb = (dx.ldb + 7) / 8 * 8;
-    sx.b_kpad8 = true;
-    if (!skinny_fits(sx) || !sk_fused_ok(dx) || !dw_wide_fits(sw) || dw.epi.mode != EPI_STORE) return NOT_TAKEN;
-  } else if (!skinny_fits(dx) || !sk_fused_ok(dx) || !dw_wide_fits(dw) || dw.epi.mode != EPI_STORE) {
-    return NOT_TAKEN;
-  }
+  if (dx.b_dw4 != dw.b_dw4) return NOT_TAKEN;
+  if (!skinny_fits(dx) || !sk_fused_ok(dx) || !dw_wide_fits(dw) || dw.epi.mode != EPI_STORE) return NOT_TAKEN;
   const SkPlan pl = sk_plan(dx);
   if (pl.splits != 1) return NOT_TAKEN;  // its reduce would follow the pair
-  if (dy_dw4 && pl.nb > 2) return NOT_TAKEN;
+  if (dx.b_dw4 && pl.nb > 2) return NOT_TAKEN;
   // the large-tile product alone on two workgroups per CU (a launch of its own is faster)
   // or with its bias on the column-sum kernel: not paired
   DlArgs d;
@@ -883,12 +876,6 @@ int run_local_dx_dw_pair(const GemmProblem &dx, const GemmProblem &dw, void *ws,
   const int n_sk = prepare_skinny(dx, pl, ws, true, &g);
   const int n_pad = (n_sk + 7) / 8 * 8;
   dw_wide_prepare(dw, n_pad, &d, &oh, &dual, &g_dl);
-  if (dy_dw4) {
-    if (oh != 128) return NOT_TAKEN;  // 256-row tiles: more pieces in flight than the counter holds
-    g.b_dw4 = 1;
-    d.dy_dw4 = 1;
-    d.dy_bytes = (uint32_t)(((int64_t)(dw.K - 1) * dw.ldb + dw.N) * 2);
-  }
   const int grid = n_pad + g_dl;
   {
     LaunchTimer t(dw.kclass, dw.layer, s);
