@@ -291,6 +291,48 @@ def test_local_bwd_dy_block_of_wider_rows(imbd, dev, col0):
     assert nrm_err(out[1][0], rdw) < 1e-5 and nrm_err(out[1][1], rdb) < 1e-5 and nrm_err(out[1][2], rdx) < 1e-5
 
 
+def test_local_step_graph_replay_matches_eager(imbd, dev):
+    """The local forward and backward calls captured into a HIP graph (as the bench times
+    them): three replays, with eager work and synchronisation between them, each give the
+    bits of the eager calls (the library enqueues only kernels on the given stream)."""
+    import torch
+    _flush("local step graph replay")
+    dout, din, b = 250, 1024, 64
+    d, W, X, DY = _local_inputs(dout, din, b, "bf16", seed=11)
+    wd, xd, dyd = _to_dev(d, "w", "bf16", dev), _to_dev(d, "x", "bf16", dev), _to_dev(d, "dy", "bf16", dev)
+    bias = dev_f32(d["b"], dev)
+    ws = torch.zeros(max(imbd.mlp_local_workspace_bytes(0, imbd.IMBD_BF16, dout, din, b),
+                         imbd.mlp_local_workspace_bytes(1, imbd.IMBD_BF16, dout, din, b), 16),
+                     dtype=torch.uint8, device=dev)
+    y = torch.empty((b, dout), dtype=torch.bfloat16, device=dev)
+    dw = torch.empty((dout, din), device=dev)
+    db = torch.empty(dout, device=dev)
+    dx = torch.empty((b, din), device=dev)
+    outs = (y, dw, db, dx)
+
+    def step(st):
+        imbd.mlp_local_fwd(wd, xd, y, 4, 16, bias=bias, relu=True, ws=ws, stream=st)
+        imbd.mlp_local_bwd(wd, dyd, xd, dw, 4, 16, db_part=db, dx_part=dx, mask_relu=True, ws=ws, stream=st)
+
+    step(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    g, cap = torch.cuda.CUDAGraph(), torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            step(cap)
+    torch.cuda.synchronize()
+    for r in range(3):
+        for o in outs:
+            o.fill_(float("nan"))
+        (wd.float() * 2.0).sum().item()   # unrelated eager work and a synchronisation
+        g.replay()
+        torch.cuda.synchronize()
+        for o, e in zip(outs, ref):
+            assert torch.equal(o, e), r
+
+
 def test_local_fwd_strided_views(imbd, dev):
     """Blocks passed as views of a larger array (leading dimension > row length)."""
     import torch
