@@ -561,7 +561,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     # The first warm-up step is kept for the parity check. The GPU reaches its steady clocks only
     # after some 20 ms of sustained work: with 5 warm-up steps the B = 256 step timed 0.213-0.215
-    # ms, with 100 or 400 0.206 ms (the same box; the seeded state timed after a warm GPU gives the
+    # ms, with 100 or 400 0.206 ms (the same GPU; the seeded state timed after a warm GPU gives the
     # warm figure too), so the default warm-up covers that time at every workload.
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="alexnet_fc_b256")
