@@ -155,6 +155,9 @@ LOCAL_SHAPES = [
     (200, 1000, 128),
     # 9 x 33 tiles of 128 x 128, ragged: the fp32 weight-gradient store on two workgroups per CU
     (1032, 4104, 72),
+    # a 500-byte Delta_Y pitch with more than 128 samples: not read in place (the paired launch
+    # takes 4-byte pieces up to 128 samples), so the block is copied into 16-byte rows first
+    (250, 512, 200),
 ]
 
 
