@@ -296,9 +296,13 @@ static int fwd_impl(const imbd_mlp_desc *d, const imbd_layer *layers, const void
     }
     TRY(gemm_run(p, part, lay.partial_bytes, s));
   }
-  return run_softmax_xent(B, d->dims[L], reinterpret_cast<const float *>(at(ws, lay.logits)), d->dims[L],
-                          labels, 1.0f / (float)B, loss, reinterpret_cast<float *>(at(ws, lay.rowloss)),
-                          at(ws, lay.dy[L]), d->dims[L], d->dtype, s, L);
+  // the batch mean of the per-sample losses rides on a later launch when the caller takes
+  // the job (the top layer's Delta_X product), else it follows here
+  float *rl = reinterpret_cast<float *>(at(ws, lay.rowloss));
+  TRY(run_softmax_xent(B, d->dims[L], reinterpret_cast<const float *>(at(ws, lay.logits)), d->dims[L], labels,
+                       1.0f / (float)B, loss, rl, at(ws, lay.dy[L]), d->dims[L], d->dtype, s, L, job == nullptr));
+  if (job) *job = LossJob{rl, loss, B, 1.0f / (float)B, true};
+  return IMBD_OK;
 }
 
 // Backward pass. A pending loss mean in *job rides on the top layer's Delta_X launch.
@@ -380,8 +384,9 @@ int mlp_bwd(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, void *ws,
   return bwd_impl(d, layers, x, ws, ws_bytes, fuse_sgd, lr, dx1, reinterpret_cast<hipStream_t>(stream), nullptr);
 }
 
-// One iteration; the loss mean travels with the top layer's Delta_X launch when both take
-// the skinny path (one launch fewer), else it gets its own launch.
+// One iteration; the loss mean travels with the top layer's Delta_X launch when that runs on
+// the skinny-batch or wide-batch kernel (one workgroup more there, one launch fewer), else
+// it gets its own launch.
 int mlp_train_step(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, const int32_t *labels,
                    void *ws, size_t ws_bytes, float lr, float *loss, void *stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);

@@ -145,9 +145,11 @@ int run_dw_wide(const GemmProblem &p, hipStream_t s);
 int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s);
 
 // ----------------------------------------------------------------- other kernels
+// mean: also launch the batch mean of the per-sample losses into *loss (else the caller
+// enqueues it later)
 int run_softmax_xent(int B, int C, const float *logits, int64_t ldz, const int32_t *labels,
                      float inv_batch, float *loss, float *row_loss, void *dz, int64_t lddz,
-                     int dz_dtype, hipStream_t s, int layer);
+                     int dz_dtype, hipStream_t s, int layer, bool mean = true);
 int run_bias_grad(int dtype, int M, int B, const void *dy, int64_t lddy, float alpha,
                   float *db_out, float *bias_sgd, float lr, hipStream_t s, int layer);
 int run_sgd(float *w, uint16_t *w16, const float *g, int64_t n, float step, hipStream_t s,

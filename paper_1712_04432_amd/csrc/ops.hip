@@ -218,7 +218,7 @@ int grid_for(int64_t work, int per_block) {
 
 int run_softmax_xent(int B, int C, const float *logits, int64_t ldz, const int32_t *labels,
                      float inv_batch, float *loss, float *row_loss, void *dz, int64_t lddz,
-                     int dz_dtype, hipStream_t s, int layer) {
+                     int dz_dtype, hipStream_t s, int layer, bool mean) {
   if (B <= 0) return IMBD_OK;
   {
     LaunchTimer t(IMBD_K_SOFTMAX, layer, s);
@@ -235,7 +235,7 @@ int run_softmax_xent(int B, int C, const float *logits, int64_t ldz, const int32
                          row_loss, dz, lddz, bf);
   }
   int rc = check_launch("softmax_xent_rows");
-  if (rc) return rc;
+  if (rc || !mean) return rc;
   return run_loss_mean(B, row_loss, inv_batch, loss, s);
 }
 
