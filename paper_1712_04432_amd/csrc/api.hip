@@ -294,6 +294,15 @@ static int fwd_impl(const imbd_mlp_desc *d, const imbd_layer *layers, const void
       *job = LossJob{rl, loss, B, 1.0f / (float)B, true};
       return IMBD_OK;
     }
+    if (i == L && wide_softmax_fits(p)) {
+      // the same past 256 samples: the wide-batch product's partials, then one pass
+      float *rl = reinterpret_cast<float *>(at(ws, lay.rowloss));
+      TRY(run_wide_softmax(p, part, lay.partial_bytes, labels, 1.0f / (float)B, rl, at(ws, lay.dy[L]), d->dims[L],
+                           d->dtype, s));
+      if (!job) return run_loss_mean(B, rl, 1.0f / (float)B, loss, s);
+      *job = LossJob{rl, loss, B, 1.0f / (float)B, true};
+      return IMBD_OK;
+    }
     TRY(gemm_run(p, part, lay.partial_bytes, s));
   }
   // the batch mean of the per-sample losses rides on a later launch when the caller takes

@@ -131,6 +131,14 @@ int run_wide(const GemmProblem &p, float *partial, int64_t ldp, int64_t sstride,
 bool skinny_softmax_fits(const GemmProblem &p);
 int run_skinny_softmax(const GemmProblem &p, void *ws, const int32_t *labels, float inv_batch, float *row_loss,
                        void *dz, int64_t lddz, int dz_dtype, hipStream_t s);
+// The same pass on split partials laid out [split][row][ldp] (the wide-batch kernel's).
+int run_softmax_rows_from_partials(const GemmProblem &p, const float *partial, int64_t ldp, int64_t sstride,
+                                   int splits, const int32_t *labels, float inv_batch, float *row_loss, void *dz,
+                                   int64_t lddz, int dz_dtype, hipStream_t s);
+// ... and for a top layer on the wide-batch kernel with K split (past 256 samples).
+bool wide_softmax_fits(const GemmProblem &p);
+int run_wide_softmax(const GemmProblem &p, void *ws, size_t ws_bytes, const int32_t *labels, float inv_batch,
+                     float *row_loss, void *dz, int64_t lddz, int dz_dtype, hipStream_t s);
 int run_loss_mean(int B, const float *row_loss, float inv_batch, float *loss, hipStream_t s);
 // The persistent fused weight-gradient + update kernel (bf16, K <= 2048): whether it
 // takes the problem, and the launch.

@@ -947,6 +947,32 @@ static int launch_reduce(const GemmProblem &p, const KArgs &g, hipStream_t s) {
   return check_launch("splitk_reduce");
 }
 
+bool wide_softmax_fits(const GemmProblem &p) {
+  const GemmPlan pl = gemm_plan(p);
+  return pl.cfg == PLAN_WIDE && pl.splits > 1 && p.a_kc && p.M <= 1024 && p.epi.mode == EPI_STORE &&
+         p.epi.relu == 0 && p.epi.mask == nullptr && p.epi.out_dtype == IMBD_F32 && p.aux_loss == nullptr &&
+         opt(IMBD_OPT_TOP_UNFUSED) == 0;
+}
+
+// The wide-batch product's split partials, then one pass per sample that adds them in split
+// order with the bias (the split reduce's arithmetic), stores the logits and takes the
+// softmax cross-entropy: the reduce launch and the softmax launch in one.
+int run_wide_softmax(const GemmProblem &p, void *ws, size_t ws_bytes, const int32_t *labels, float inv_batch,
+                     float *row_loss, void *dz, int64_t lddz, int dz_dtype, hipStream_t s) {
+  const GemmPlan pl = gemm_plan(p);
+  if (ws == nullptr || ws_bytes < pl.ws_bytes || (uintptr_t)ws % 16 != 0) {
+    set_error("top-layer product %dx%dx%d needs %zu bytes of 16-byte aligned workspace, got %zu", p.M, p.N, p.K,
+              pl.ws_bytes, ws_bytes);
+    return IMBD_EWORKSPACE;
+  }
+  float *partial = reinterpret_cast<float *>(ws);
+  const int64_t ldp = partial_ld(p.M), sstride = partial_split_stride(p.M, p.N);
+  const int rc = run_wide(p, partial, ldp, sstride, s);
+  if (rc != IMBD_OK) return rc;
+  return run_softmax_rows_from_partials(p, partial, ldp, sstride, pl.splits, labels, inv_batch, row_loss, dz, lddz,
+                                        dz_dtype, s);
+}
+
 int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   if (p.db_mode != 0 && p.b_kc) {
     set_error("bias sums need the B operand stored [k][n]");

@@ -557,6 +557,7 @@ __global__ void __launch_bounds__(256) skinny_reduce(SkReduceArgs g) {
 struct SkSoftmaxArgs {
   const float *partial;
   int64_t tpitch, sstride;
+  int64_t ldp;    // > 0: partials laid out [split][row][ldp] (the wide-batch kernel's), else per tile
   int splits, B, C;
   float alpha;
   const float *bias;
@@ -583,7 +584,8 @@ __global__ void __launch_bounds__(1024) skinny_softmax_rows(SkSoftmaxArgs g) {
   const bool in = c < g.C;
   float z = -INFINITY;
   if (in) {
-    const float *p = g.partial + (int64_t)(c >> 6) * g.tpitch + row * 64 + (c & 63);
+    const float *p = g.ldp > 0 ? g.partial + (int64_t)row * g.ldp + c
+                               : g.partial + (int64_t)(c >> 6) * g.tpitch + row * 64 + (c & 63);
     float a = p[0];
     for (int q0 = 1; q0 < g.splits; q0 += 8) {
       float t[8];
@@ -828,6 +830,7 @@ int run_skinny_softmax(const GemmProblem &p, void *ws, const int32_t *labels, fl
   a.partial = g.partial;
   a.tpitch = g.tpitch;
   a.sstride = g.sstride;
+  a.ldp = 0;
   a.splits = g.splits;
   a.B = p.N;
   a.C = p.M;
@@ -847,6 +850,35 @@ int run_skinny_softmax(const GemmProblem &p, void *ws, const int32_t *labels, fl
     hipLaunchKernelGGL(skinny_softmax_rows, dim3(p.N), dim3(threads), 0, s, a);
   }
   return check_launch("skinny_softmax_rows");
+}
+
+int run_softmax_rows_from_partials(const GemmProblem &p, const float *partial, int64_t ldp, int64_t sstride,
+                                   int splits, const int32_t *labels, float inv_batch, float *row_loss, void *dz,
+                                   int64_t lddz, int dz_dtype, hipStream_t s) {
+  SkSoftmaxArgs a;
+  a.partial = partial;
+  a.tpitch = 0;
+  a.sstride = sstride;
+  a.ldp = ldp;
+  a.splits = splits;
+  a.B = p.N;
+  a.C = p.M;
+  a.alpha = p.epi.alpha;
+  a.bias = p.epi.bias;
+  a.logits = reinterpret_cast<float *>(p.epi.out);
+  a.ldz = p.epi.ldo;
+  a.labels = labels;
+  a.inv_batch = inv_batch;
+  a.row_loss = row_loss;
+  a.dz = dz;
+  a.lddz = lddz;
+  a.dz_bf16 = dz_dtype == IMBD_BF16 ? 1 : 0;
+  {
+    LaunchTimer t(IMBD_K_SOFTMAX, p.layer, s);
+    const int threads = (p.M + 63) / 64 * 64;
+    hipLaunchKernelGGL(skinny_softmax_rows, dim3(p.N), dim3(threads), 0, s, a);
+  }
+  return check_launch("softmax_rows_from_partials");
 }
 
 size_t skinny_ws_bytes(const GemmProblem &p) {

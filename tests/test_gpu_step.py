@@ -404,3 +404,32 @@ def test_alexnet_local_4x16_blocks_full_size(imbd, dev):
             rdx = oracle.relu_mask(oracle.input_grad(W, DY[rows]), X[rows])
             assert nrm_err(host(dx)[rows], rdx) < 1e-4
 
+
+
+def test_wide_top_layer_softmax_one_pass_matches_two(imbd, dev):
+    """Past 256 samples the top layer's K-split partials go straight into the softmax pass
+    (one launch for the split reduce and the softmax cross-entropy). Against the reduce and
+    the row softmax as two launches (option top_unfused): the logits bit for bit (the same
+    split-order sum and bias), the per-sample losses, the loss and Delta_Y of the top layer
+    within fp32 rounding of the two summation orders, and both against the oracle."""
+    import torch
+    cfg = scaled_mlp((2048, 2048, 1000), 512, "bf16")
+    _flush("wide top layer: softmax in one pass vs two")
+    d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev, seed=4)
+    out = {}
+    for unfused in (0, 1):
+        with imbd.options(top_unfused=unfused):
+            imbd.timing_begin(imbd.IMBD_K_SPLITK, -1, 16)
+            imbd.mlp_fwd(net, layers, x, lab, ws, loss)
+            n_red, _ = imbd.timing_end()
+        torch.cuda.synchronize()
+        out[unfused] = (host(imbd.ws_view(net, ws, imbd.IMBD_WS_LOGITS)), loss.item(),
+                        host(imbd.ws_view(net, ws, imbd.IMBD_WS_DY, 2)), n_red)
+    # two K-split reduces of the hidden layers either way; the top layer's only when unfused
+    assert out[1][3] == out[0][3] + 1, (out[0][3], out[1][3])
+    assert np.array_equal(out[0][0], out[1][0])
+    assert abs(out[0][1] - out[1][1]) <= 1e-6 * abs(out[1][1])
+    assert nrm_err(out[0][2], out[1][2]) < 1e-5
+    ref = oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, "bf16")
+    assert abs(out[0][1] - ref["loss"]) < TOL_BF16 * abs(ref["loss"])
+    assert nrm_err(out[0][0], ref["logits"]) < TOL_BF16
