@@ -257,7 +257,9 @@ enum imbd_option {
     IMBD_OPT_DW_GENERIC = 7,    /* 1: the fused update on the tiled template */
     IMBD_OPT_GEMM_CFG = 8,      /* tile configuration of the tiled template, -1 = planned (-1..3) */
     IMBD_OPT_GEMM_SPLITS = 9,   /* K split of the tiled template, 0 = planned */
-    IMBD_OPT_CONV_NT = 10,      /* 0: the conv tile on the tiled template */
+    IMBD_OPT_CONV_NT = 10,      /* 0: the conv tile on the tiled template; 1: on the large-tile
+                                   kernels, tile height planned (default); 2 / 3: with tiles of
+                                   128 / 112 output positions */
     IMBD_OPT_SKINNY_NB = 11,    /* samples per workgroup of the B <= 256 product kernel, in units
                                    of 64 (1, 2 or 4), 0 = planned */
     IMBD_OPT_DW_WIDE_DUAL = 12, /* the large-tile fused update with two workgroups per CU

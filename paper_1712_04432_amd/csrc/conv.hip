@@ -10,19 +10,21 @@
 // operand is 64 contiguous channels of shifted rows.
 //
 // The products are MFMA-bound (2 x 9 x C flops per output), so a workgroup owns a large
-// tile: 128 output positions x all 256 channels over the whole K = 9 C (no split, no
-// partials; the epilogue writes the outputs). With one workgroup per CU, the tiles of a
+// tile: 128 (or 112) output positions x all 256 channels over the whole K = 9 C (no split,
+// no partials; the epilogue writes the outputs). With one workgroup per CU, the tiles of a
 // short last round run as two 128-channel halves each (the loader and MMA waves of the
 // other half only keep the slab barriers). The kernel keeps the layout of the skinny-batch
 // kernel (csrc/skinny.hip): both operands travel through LDS in 64-k slabs written by
 // buffer loads that go straight to LDS in whole 128-byte lines, loader waves with their
 // own memory counters, one barrier per slab, XOR-swizzled 16-byte chunks:
-//  * waves 8-9 stream the activation slab (128 shifted rows x 128 B) through a 4-slot ring;
+//  * waves 8-9 stream the activation slab (128 or 112 shifted rows x 128 B) through a
+//    4-slot ring;
 //  * waves 10-11 stream the weight slab (256 channels x 64 k) through a 3-slot ring: rows
 //    of W for the forward pass, k-rows of W (64 output channels of one tap x 256 input
 //    channels, as four 64-channel quarters) for the input gradient, whose fragments then
 //    come from the gfx950 LDS transpose read;
-//  * waves 0-7, two per SIMD, each accumulate 64 positions x 64 channels in registers.
+//  * waves 0-7, two per SIMD, each accumulate 64 (or 48) positions x 64 channels in
+//    registers.
 // After the last slab the tile goes through LDS ([position][channel], fp32) and is written
 // as whole 512-byte (bf16) or 1 KB (fp32) output rows.
 
@@ -33,12 +35,11 @@
 namespace imbd {
 namespace {
 
-constexpr int CV_BM = 128;             // positions per workgroup
+constexpr int CV_BM = 128;             // positions per workgroup (at most; 112 with FM = 7)
 constexpr int CV_BN = 256;             // channels of the output per workgroup
 constexpr int CV_KS = 64;              // k per slab: 64 channels of one tap
 constexpr int CV_NA = 4;               // activation ring slots
 constexpr int CV_NW = 3;               // weight ring slots
-constexpr int CV_ASLOT = CV_BM * 128;  // 16 KB
 constexpr int CV_WSLOT = CV_BN * 128;  // 32 KB
 constexpr int CV_QSLOT = 64 * 128;     // one 64-channel quarter of a transposed weight slab
 constexpr int CV_PITCH = CV_BN + 4;    // staging row pitch in floats (1040 B)
@@ -57,21 +58,28 @@ struct CvArgs {
 __device__ __forceinline__ int cv_swz_kc(int r) { return r & 7; }
 __device__ __forceinline__ int cv_swz_tr(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }
 
-// TR: input gradient (W read transposed); else forward. Eight MMA waves, two per SIMD, so
-// that one computes while the other waits for its fragments or the slab barrier (with one
-// per SIMD the matrix pipe was busy ~40% of the time): wave w takes the positions of half
-// w%2 and the channels of quarter w/2. The loader waves follow the MMA waves.
-template <bool TR>
+// TR: input gradient (W read transposed); else forward. FM: 16-position blocks per tile
+// (8: 128 positions; 7: 112, whose tile count fills the chip's rounds better for some
+// grids). Eight MMA waves, two per SIMD, so that one computes while the other waits for
+// its fragments or the slab barrier (with one per SIMD the matrix pipe was busy ~40% of
+// the time); each takes one position half (blocks 0-3 or 4..FM-1) and one channel
+// quarter. Waves w and w+4 share a SIMD: with FM = 8 wave w takes position half w%2 and
+// quarter w/2; with FM = 7 the two waves of a SIMD take different position halves (4 + 3
+// blocks on every SIMD), and each channel half (the quarters of a half tile) still spans
+// all four SIMDs. The loader waves follow the MMA waves.
+template <bool TR, int FM>
 __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
+  static_assert(FM == 8 || FM == 7, "tile");
   constexpr int NMW = 8;
-  constexpr int FM = 8, BM = 16 * FM;  // 128 positions
+  constexpr int BM = 16 * FM;
   constexpr int NT = 64 * (NMW + 4);
-  constexpr int FMW = FM / 2;          // position blocks per MMA wave
+  constexpr int FMW = 4;               // position blocks per MMA wave (at most)
   constexpr uint32_t OOB = 0x80000000u;
-  constexpr int WRING = CV_NW * CV_WSLOT, ARING = CV_NA * CV_ASLOT;
+  constexpr int ASLOT = BM * 128;
+  constexpr int WRING = CV_NW * CV_WSLOT, ARING = CV_NA * ASLOT;
   __shared__ __attribute__((aligned(1024))) char smem[WRING + ARING];
   static_assert(WRING + ARING <= 160 * 1024, "LDS");
-  static_assert(CV_BM * CV_PITCH * 4 <= WRING + ARING, "staging");
+  static_assert(BM * CV_PITCH * 4 <= WRING + ARING, "staging");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -172,7 +180,7 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
     }
     const uint32_t d0 = ldsa + (uint32_t)(FM * aw * 1024);
     auto issue = [&](int S) {
-      const uint32_t slot = d0 + (uint32_t)((S % CV_NA) * CV_ASLOT);
+      const uint32_t slot = d0 + (uint32_t)((S % CV_NA) * ASLOT);
       uint32_t off = OOB;
       if (S < nsl) {
         int c0;
@@ -198,9 +206,12 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
   } else {
     // --------------------------------------------------------------- MMA group
     const int fi = lane & 15, kg = lane >> 4;
-    const int nq = wave >> 1;          // channel quarter of the wave
-    const int mb0 = FMW * (wave & 1);  // first position block
-    const int nb0 = 4 * nq;                                // first 16-channel block
+    const int sim = wave & 3, j4 = wave >> 2;
+    const int nq = FM == 8 ? wave >> 1 : 2 * j4 + (sim >> 1);    // channel quarter of the wave
+    const int ph = FM == 8 ? wave & 1 : (sim & 1) ^ j4;          // position half
+    const int mb0 = FMW * ph;                                    // first position block
+    const int nbw = ph == 0 ? FMW : FM - FMW;                    // its position blocks
+    const int nb0 = 4 * nq;                                      // first 16-channel block
     uint32_t fa[FMW], fx[4];
 #pragma unroll
     for (int i = 0; i < FMW; ++i) fa[i] = (uint32_t)((16 * (mb0 + i) + fi) * 128);
@@ -229,7 +240,8 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
       const uint32_t co = (uint32_t)(((4 * s + kg) ^ sw) * 16);
 #pragma unroll
       for (int i = 0; i < FMW; ++i)
-        ad[i] = __builtin_bit_cast(bf16x8, *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(as + fa[i] + co));
+        if (i < nbw)
+          ad[i] = __builtin_bit_cast(bf16x8, *(const __attribute__((address_space(3))) u32x4 *)(uintptr_t)(as + fa[i] + co));
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         if constexpr (!TR) {
@@ -245,8 +257,9 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
     auto mma = [&](const bf16x8 (&af)[FMW], const bf16x8 (&wf)[4]) {
 #pragma unroll
       for (int i = 0; i < FMW; ++i)
+        if (i < nbw)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], wf[j], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], wf[j], acc[i][j], 0, 0, 0);
     };
 
     uint32_t as = ldsa, ws = ldsw;  // slots of the slab being read
@@ -258,7 +271,7 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
       mma(av[0], wv[0]);
       __builtin_amdgcn_sched_barrier(0);
       lds_barrier();  // B_{S+1}: every read of slab S has landed; publish S+1, free S
-      as = ldsa + (uint32_t)(((S + 1) % CV_NA) * CV_ASLOT);
+      as = ldsa + (uint32_t)(((S + 1) % CV_NA) * ASLOT);
       ws = ldsw + (uint32_t)(((S + 1) % CV_NW) * CV_WSLOT);
       read(as, ws, 0, av[0], wv[0]);  // past the last slab this reads a spent slot, unused
       __builtin_amdgcn_sched_barrier(0);
@@ -271,10 +284,11 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
     float *stg = reinterpret_cast<float *>(smem);
 #pragma unroll
     for (int i = 0; i < FMW; ++i)
+      if (i < nbw)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) stg[(16 * (mb0 + i) + 4 * kg + e) * CV_PITCH + 16 * (nb0 + j) + fi] = acc[i][j][e];
+          for (int e = 0; e < 4; ++e) stg[(16 * (mb0 + i) + 4 * kg + e) * CV_PITCH + 16 * (nb0 + j) + fi] = acc[i][j][e];
   }
   lds_barrier();
   // ---- write the tile's rows (output position p is row p of the output); a half tile
@@ -608,18 +622,39 @@ int run_conv_nt(int pass, int N, int H, int W, int Ci, int Co, const void *act, 
   a.Ck = pass == 1 ? Ci : Co;
   a.Cw = Ci;
   a.M = N * H * W;
-  a.tiles = (a.M + CV_BM - 1) / CV_BM;
   // One workgroup per CU (160 KB of LDS): past one round, the tiles of a short last round
-  // run as 128-channel halves on twice as many CUs, which ends that round sooner.
-  const int last = a.tiles > CV_CUS ? a.tiles % CV_CUS : 0;
-  const bool halves = last > 0 && 2 * last <= CV_CUS;
+  // run as 128-channel halves on twice as many CUs, which ends that round sooner. The tile
+  // height (128 or 112 positions) is the one whose rounds (a round of halves counted as
+  // half a round) take fewer position blocks per CU: on the 32 x 56 x 56 grid, 784 tiles
+  // of 128 (3 rounds and a short one) against 896 of 112 (3 rounds and a full round of
+  // halves).
+  auto plan = [&](int fm, int *tiles, int *last, bool *halves) {
+    *tiles = (a.M + 16 * fm - 1) / (16 * fm);
+    *last = *tiles > CV_CUS ? *tiles % CV_CUS : 0;
+    *halves = *last > 0 && 2 * *last <= CV_CUS;
+    const int rounds = (*tiles + CV_CUS - 1) / CV_CUS;
+    return (*halves ? 2 * rounds - 1 : 2 * rounds) * fm;  // in half rounds x blocks
+  };
+  int t8, l8, t7, l7;
+  bool h8, h7;
+  const int c8 = plan(8, &t8, &l8, &h8), c7 = plan(7, &t7, &l7, &h7);
+  const int o = opt(IMBD_OPT_CONV_NT);
+  const int fm = o == 2 ? 8 : o == 3 ? 7 : (c7 < c8 ? 7 : 8);
+  a.tiles = fm == 8 ? t8 : t7;
+  const int last = fm == 8 ? l8 : l7;
+  const bool halves = fm == 8 ? h8 : h7;
   a.tfull = halves ? a.tiles - last : a.tiles;
   a.gfull = (a.tfull + 7) / 8 * 8;
   const int grid = a.gfull + (halves ? 2 * last : 0);
   {
     LaunchTimer t(pass == 1 ? IMBD_K_CONV_FWD : IMBD_K_CONV_DGRAD, 0, s);
-    if (pass == 1) hipLaunchKernelGGL(conv_nt_kernel<false>, dim3(grid), dim3(768), 0, s, a);
-    else hipLaunchKernelGGL(conv_nt_kernel<true>, dim3(grid), dim3(768), 0, s, a);
+    if (pass == 1) {
+      if (fm == 8) hipLaunchKernelGGL((conv_nt_kernel<false, 8>), dim3(grid), dim3(768), 0, s, a);
+      else hipLaunchKernelGGL((conv_nt_kernel<false, 7>), dim3(grid), dim3(768), 0, s, a);
+    } else {
+      if (fm == 8) hipLaunchKernelGGL((conv_nt_kernel<true, 8>), dim3(grid), dim3(768), 0, s, a);
+      else hipLaunchKernelGGL((conv_nt_kernel<true, 7>), dim3(grid), dim3(768), 0, s, a);
+    }
   }
   return check_launch("conv_nt");
 }

@@ -32,7 +32,7 @@ const OptionDef kOptions[IMBD_OPT_COUNT] = {
     {"IMBD_DW_GENERIC", 0, 0, 1},        // fused update on the tiled template
     {"IMBD_GEMM_CFG", -1, -1, 3},        // tiled template's tile configuration (-1: planner)
     {"IMBD_GEMM_SPLITS", 0, 0, 4096},    // tiled template's K split (0: planner)
-    {"IMBD_CONV_NT", 1, 0, 1},           // conv tile on the large-tile kernels
+    {"IMBD_CONV_NT", 1, 0, 3},           // conv tile: 0 tiled template, 1 planned, 2 / 3 128 / 112 positions
     {"IMBD_SKINNY_NB", 0, 0, 4},         // skinny kernel's samples per workgroup / 64 (0: planner)
     {"IMBD_DW_WIDE_DUAL", -1, -1, 1},    // large-tile fused update, two workgroups per CU (-1: planner)
     {"IMBD_LOCAL_PAIR", 1, 0, 1},        // local backward: Delta_X and Delta_W products in one launch

@@ -117,9 +117,9 @@ def test_conv_tile_full_size_every_element(imbd, dev):
 
 
 def test_conv_tile_128_position_tiles_sampled(imbd, dev):
-    """A tile size for which the forward kernel takes 128-position tiles (240 tiles fill
-    one round of workgroups; 112-position tiles would need two): sampled outputs of the
-    three passes."""
+    """A tile size for which the forward kernel plans 128-position tiles (225 tiles fill
+    one round of workgroups; 258 tiles of 112 positions would need a second, short one):
+    sampled outputs of the three passes."""
     _flush("conv 8x60x60 128->256")
     N, H, W, Ci, Co = 8, 60, 60, 128, 256
     d = make_conv_inputs(N, H, W, Ci, Co, seed=9, border=(True, False, False, True))
@@ -137,12 +137,15 @@ def test_conv_tile_128_position_tiles_sampled(imbd, dev):
 
 
 @pytest.mark.parametrize("N,H,W", [(4, 92, 92), (4, 113, 113)])
-def test_conv_tile_last_round_sampled(imbd, dev, N, H, W):
-    """More 128-position tiles than one round of workgroups on 256 CUs: 4 x 92 x 92 has
-    265 tiles, whose last 9 run as 128-channel halves (18 workgroups); 4 x 113 x 113 has
-    400, whose last 144 run whole. Every channel of rows in the last round's tiles and
-    random outputs elsewhere, fp32 and bf16 outputs, forward and input gradient."""
-    _flush(f"conv last round {(N, H, W)}")
+@pytest.mark.parametrize("tile", [128, 112])
+def test_conv_tile_last_round_sampled(imbd, dev, N, H, W, tile):
+    """More tiles than one round of workgroups on 256 CUs, both tile heights forced:
+    4 x 92 x 92 has 265 tiles of 128 positions, whose last 9 run as 128-channel halves (18
+    workgroups), or 303 of 112, whose last 47 run as halves; 4 x 113 x 113 has 400 of 128
+    (457 of 112), whose last 144 (201) run whole. Every channel of rows in the last round's
+    tiles and random outputs elsewhere, fp32 and bf16 outputs, forward and input
+    gradient."""
+    _flush(f"conv last round {(N, H, W)} tile {tile}")
     C = 256
     d = make_conv_inputs(N, H, W, C, C, seed=H, border=(True, True, False, False))
     xv, wv, dyv = bf16_values(d["x_bits"]), bf16_values(d["w_bits"]), bf16_values(d["dy_bits"])
@@ -154,12 +157,39 @@ def test_conv_tile_last_round_sampled(imbd, dev, N, H, W):
     ry = oracle.conv3x3_fwd_at(xv, wv, idx)
     rx = oracle.conv3x3_dgrad_at(dyv, wv, idx)
     for out_bf16 in (False, True):
-        y, dx, _ = _run(imbd, dev, d, out_bf16=out_bf16)
+        with imbd.options(conv_nt=2 if tile == 128 else 3):
+            y, dx, _ = _run(imbd, dev, d, out_bf16=out_bf16)
         tol = 2.0 ** -8 + 1e-5 if out_bf16 else 1e-5
         assert nrm_err(host(y).reshape(-1)[idx], ry) < tol
         assert nrm_err(host(dx).reshape(-1)[idx], rx) < tol
         import torch
         assert torch.isfinite(y).all().item() and torch.isfinite(dx).all().item()
+
+
+def test_conv_tile_heights_agree_bitwise(imbd, dev):
+    """The 32 x 56 x 56 tile, 256 -> 256 channels, forward and input gradient with tiles of
+    128 positions (784 tiles: three rounds and a short one of 128-channel halves) and of
+    112 (896: three rounds and a full round of halves): every output is the same sum in
+    the same slab and MFMA order, so the two give identical bits, fp32 and bf16."""
+    import torch
+    _flush("conv tile heights 128 / 112, full size")
+    N, H, W, C = 32, 56, 56, 256
+    d = make_conv_inputs(N, H, W, C, C, seed=11, border=(False, True, False, True))
+    x = dev_bf16_bits(d["x_bits"], dev)
+    w = dev_bf16_bits(d["w_bits"], dev)
+    dy = dev_bf16_bits(d["dy_bits"], dev)
+    for odt in (torch.float32, torch.bfloat16):
+        outs = []
+        for o in (2, 3):
+            y = torch.full((N, H, W, C), float("nan"), dtype=odt, device=dev)
+            dx = torch.full((N, H, W, C), float("nan"), dtype=odt, device=dev)
+            with imbd.options(conv_nt=o):
+                imbd.conv3x3_tile_fwd(x, w, y)
+                imbd.conv3x3_tile_dgrad(dy, w, dx)
+            torch.cuda.synchronize()
+            outs.append((y, dx))
+        assert torch.isfinite(outs[0][0]).all().item() and torch.isfinite(outs[0][1]).all().item()
+        assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
 
 
 def test_conv_stitched_domain_split(imbd, dev):
