@@ -329,31 +329,57 @@ __global__ void __launch_bounds__(768, 1) conv_nt_kernel(CvArgs a) {
 
 
 // ------------------------------------------------------------------ weight gradient
-// dW[o][tap][c] = sum_P dy[P][o] * x_pad[P + r*(W+2) + s][c] over the positions P of the
-// padded grid whose row and column are inside the tile (Sec. 2.2: the tile's partial of
+// dW[o][tap][c] = sum_p dy[p][o] * x_pad[P(p) + r*(W+2) + s][c] over the tile's output
+// positions p = (n, h, w), P(p) = (n (H+2) + h) (W+2) + w (Sec. 2.2: the tile's partial of
 // the weight gradient, which the all-reduce over the domain completes). Both operands are
 // position-major, so K = positions and both fragments come from k-row-major LDS slabs
 // through the transpose read. A workgroup owns 256 output channels x 128 input channels
-// of one tap over one range of positions; the ranges are K splits whose fp32 partials the
-// split-K reduce adds in split order. Slabs of 64 positions:
+// of one tap over one range of output positions; the ranges are K splits whose fp32
+// partials the split-K reduce adds in split order. Slabs of 64 positions, each row's
+// padded-grid row P(p) kept incrementally by the loader lane that fetches it:
 //  * waves 6-7 load the Delta_Y slab (64 positions x 256 channels, four 64-channel
-//    quarters), rows of positions outside the tile's interior replaced by zeros (their
-//    loads are out of range);
+//    quarters);
 //  * waves 4-5 load the shifted activation slab (64 positions x 128 channels);
 //  * waves 0-3 each accumulate 128 output channels x 64 input channels.
+// Rows past the split's range read as zero (their loads are out of range).
 struct CwArgs {
   const uint16_t *x;    // x_pad [N][H+2][W+2][Ci]
   const uint16_t *dy;   // interior start of dy_pad: dy_pad + ((W+2) + 1) * Co
   float *partial;       // [split][Co][ldp]: element (tap*Ci + c, o) at o*ldp + tap*Ci + c
   int64_t ldp, sstride;
   int H, W, Ci, Co;
-  int M, k_split, splits, tiles;  // positions (up to the last interior one); tiles = 9 * Ci / 128
+  int M, k_split, splits, tiles;  // output positions N*H*W; tiles = 9 * Ci / 128
+  int Mp;                         // padded-grid rows up to the last output position's
 };
 
 constexpr int CW_XSLOT = 64 * 256;   // 16 KB: 64 positions x 128 channels
 constexpr int CW_DSLOT = 64 * 512;   // 32 KB: 64 positions x 256 channels
 constexpr int CW_NX = 4, CW_ND = 3;  // ring slots
 constexpr int CW_PITCH = 128 + 4;    // staging row pitch in floats
+
+// Output position p as (h, w) and its padded-grid row P(p); the step to position p + 64
+// without a division (the rows that wrap past an image row or an image are counted).
+__device__ __forceinline__ void cw_row_init(const CwArgs &a, int p, int *h, int *w, int *P) {
+  const int HW = a.H * a.W, n = p / HW, rem = p - n * HW;
+  *h = rem / a.W;
+  *w = rem - *h * a.W;
+  *P = (n * (a.H + 2) + *h) * (a.W + 2) + *w;
+}
+__device__ __forceinline__ void cw_row_next(const CwArgs &a, int *h, int *w, int *P) {
+  const int Wp = a.W + 2, dh = 64 / a.W, dw = 64 - dh * a.W;
+  *w += dw;
+  *h += dh;
+  *P += dh * Wp + dw;
+  if (*w >= a.W) {
+    *w -= a.W;
+    ++*h;
+    *P += 2;
+  }
+  while (*h >= a.H) {
+    *h -= a.H;
+    *P += 2 * Wp;
+  }
+}
 
 __global__ void __launch_bounds__(512, 1) conv_wg_kernel(CwArgs a) {
   constexpr uint32_t OOB = 0x80000000u;
@@ -373,7 +399,7 @@ __global__ void __launch_bounds__(512, 1) conv_wg_kernel(CwArgs a) {
   const int tap = tile / (a.Ci / 128), c0 = (tile - tap * (a.Ci / 128)) * 128;
   const int klo = split * a.k_split, krange = min(a.M, klo + a.k_split) - klo;
   const int nsl = krange > 0 ? (krange + 63) / 64 : 0;
-  const int Wp = a.W + 2, HWp = (a.H + 2) * Wp;
+  const int Wp = a.W + 2;
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
   const uint32_t ldsd = lds0, ldsx = lds0 + DRING;
 
@@ -381,41 +407,30 @@ __global__ void __launch_bounds__(512, 1) conv_wg_kernel(CwArgs a) {
     // ---------------------------------------------------- Delta_Y loaders (6, 7)
     // blocks 16dw..16dw+15 of a slot: quarter h = blk/8, k-rows 8(blk%8)..+7
     const int dw = wave - 6;
-    const i32x4 rd = buf_rsrc(a.dy, (uint32_t)((int64_t)a.M * a.Co * 2));
+    const i32x4 rd = buf_rsrc(a.dy, (uint32_t)((int64_t)a.Mp * a.Co * 2));
     // the wave's blocks cover quarters 2dw, 2dw+1 of the same 8 row groups g (k-rows
-    // 8g + lane/8); each row's (row, column) in the padded image advances by 64 positions
-    // per slab, kept incrementally (no division per slab)
+    // 8g + lane/8)
     uint32_t col[2][8];
-    int hh[8], ww[8];
+    int hh[8], ww[8], pp[8];
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
       const int r = 8 * g + (lane >> 3);
       const int c = (lane & 7) ^ cv_swz_tr(r);
       col[0][g] = (uint32_t)((64 * (2 * dw) + 8 * c) * 2);
       col[1][g] = (uint32_t)((64 * (2 * dw + 1) + 8 * c) * 2);
-      const int rem = (klo + r) % HWp;
-      hh[g] = rem / Wp;
-      ww[g] = rem - hh[g] * Wp;
+      cw_row_init(a, klo + r, &hh[g], &ww[g], &pp[g]);
     }
-    const int adv_h = 64 / Wp, adv_w = 64 - adv_h * Wp, Hp = a.H + 2;
     auto issue = [&](int S) {
       const uint32_t slot = ldsd + (uint32_t)((S % CW_ND) * CW_DSLOT);
 #pragma unroll
       for (int g = 0; g < 8; ++g) {
-        const int r = 8 * g + (lane >> 3), P = klo + S * 64 + r;
-        const bool ok = S < nsl && S * 64 + r < krange && hh[g] < a.H && ww[g] < a.W;
-        const uint32_t off = (uint32_t)P * (uint32_t)(a.Co * 2);
+        const int r = 8 * g + (lane >> 3);
+        const bool ok = S < nsl && S * 64 + r < krange;
+        const uint32_t off = (uint32_t)pp[g] * (uint32_t)(a.Co * 2);
 #pragma unroll
         for (int hq = 0; hq < 2; ++hq)
           dma16(rd, ok ? off + col[hq][g] : OOB, slot + (uint32_t)((2 * dw + hq) * CV_QSLOT + g * 1024));
-        // the same row of the next slab: 64 positions on
-        ww[g] += adv_w;
-        hh[g] += adv_h;
-        if (ww[g] >= Wp) {
-          ww[g] -= Wp;
-          ++hh[g];
-        }
-        while (hh[g] >= Hp) hh[g] -= Hp;
+        cw_row_next(a, &hh[g], &ww[g], &pp[g]);
       }
     };
 #pragma unroll
@@ -430,21 +445,27 @@ __global__ void __launch_bounds__(512, 1) conv_wg_kernel(CwArgs a) {
     // quarter h = blk/8 (channels c0 + 64h ..), k-rows 8(blk%8).. of positions shifted by tap
     const int xw = wave - 4;
     const int r3 = tap / 3, s3 = tap - 3 * r3, shift = r3 * Wp + s3;
-    const i32x4 rx = buf_rsrc(a.x, (uint32_t)((int64_t)(a.M + 2 * Wp + 2) * a.Ci * 2));
-    uint32_t base[8], dst[8];
+    const i32x4 rx = buf_rsrc(a.x, (uint32_t)((int64_t)(a.Mp + 2 * Wp + 2) * a.Ci * 2));
+    // block q of the wave's quarter: k-rows 8q + lane/8
+    uint32_t col[8];
+    int hh[8], ww[8], pp[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      const int blk = 8 * xw + q, g = blk & 7;
-      const int r = 8 * g + (lane >> 3);
+      const int r = 8 * q + (lane >> 3);
       const int c = (lane & 7) ^ cv_swz_tr(r);
-      base[q] = (uint32_t)(((int64_t)(klo + r + shift) * a.Ci + c0 + 64 * xw + 8 * c) * 2);
-      dst[q] = (uint32_t)(xw * CV_QSLOT + g * 1024);
+      col[q] = (uint32_t)((c0 + 64 * xw + 8 * c) * 2);
+      cw_row_init(a, klo + r, &hh[q], &ww[q], &pp[q]);
     }
-    const uint32_t sstep = (uint32_t)(64 * a.Ci * 2);
     auto issue = [&](int S) {
-      const uint32_t slot = ldsx + (uint32_t)((S % CW_NX) * CW_XSLOT);
+      const uint32_t slot = ldsx + (uint32_t)((S % CW_NX) * CW_XSLOT) + (uint32_t)(xw * CV_QSLOT);
 #pragma unroll
-      for (int q = 0; q < 8; ++q) dma16(rx, S < nsl ? base[q] + (uint32_t)S * sstep : OOB, slot + dst[q]);
+      for (int q = 0; q < 8; ++q) {
+        const int r = 8 * q + (lane >> 3);
+        const bool ok = S < nsl && S * 64 + r < krange;
+        const uint32_t off = (uint32_t)(pp[q] + shift) * (uint32_t)(a.Ci * 2);
+        dma16(rx, ok ? off + col[q] : OOB, slot + (uint32_t)(q * 1024));
+        cw_row_next(a, &hh[q], &ww[q], &pp[q]);
+      }
     };
 #pragma unroll
     for (int S = 0; S < CW_NX - 1; ++S) issue(S);
@@ -576,7 +597,7 @@ bool conv_wg_fits(int N, int H, int W, int Ci, int Co, const void *x, const void
 }
 
 void conv_wg_plan(int N, int H, int W, int Ci, int *splits, int *k_split) {
-  const int64_t M = (int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W;
+  const int64_t M = (int64_t)N * H * W;
   const int tiles = 9 * Ci / 128;
   int s = 256 / tiles;
   if (s < 1) s = 1;
@@ -598,7 +619,8 @@ int run_conv_wg(int N, int H, int W, int Ci, int Co, const void *x, const void *
   a.W = W;
   a.Ci = Ci;
   a.Co = Co;
-  a.M = (int)((int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W);
+  a.M = N * H * W;
+  a.Mp = (int)((int64_t)(N - 1) * (H + 2) * (W + 2) + (int64_t)(H - 1) * (W + 2) + W);
   conv_wg_plan(N, H, W, Ci, &a.splits, &a.k_split);
   a.tiles = 9 * Ci / 128;
   const int grid = (a.tiles * a.splits + 7) / 8 * 8;

@@ -49,7 +49,7 @@ def _run(imbd, dev, d, out_bf16=False):
                                          (1, 2, 3, 256, 256), (2, 5, 7, 64, 256), (3, 20, 20, 64, 256),
                                          (1, 6, 11, 256, 64), (2, 7, 9, 256, 128),
                                          # C_in a multiple of 128 as well: the split-K weight-gradient
-                                         # kernel (one split of 8 positions; 22 splits)
+                                         # kernel (two splits, the last of 6 positions; 19 splits)
                                          (2, 5, 7, 128, 256), (3, 20, 20, 128, 256)])
 @pytest.mark.parametrize("border", [(False, False, False, False), (True, False, True, False),
                                     (True, True, True, True)])
