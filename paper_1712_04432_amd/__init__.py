@@ -23,7 +23,7 @@ from ._abi import IMBD_STATIC_SCRATCH_BYTES  # noqa: F401
 from ._abi import (IMBD_OPT_CONV_NT, IMBD_OPT_COUNT, IMBD_OPT_DW_GENERIC, IMBD_OPT_DW_STREAM,  # noqa: F401
                    IMBD_OPT_DW_WIDE_DUAL, IMBD_OPT_DW_WIDE_MIN_K, IMBD_OPT_LOCAL_PAIR, IMBD_OPT_GEMM_CFG, IMBD_OPT_GEMM_SPLITS, IMBD_OPT_SKINNY_OFF,
                    IMBD_OPT_SKINNY_NB, IMBD_OPT_SKINNY_SPLITS, IMBD_OPT_TOP_UNFUSED, IMBD_OPT_WIDE_OFF,
-                   IMBD_OPT_WIDE_SPLITS)
+                   IMBD_OPT_WIDE_SPLITS, IMBD_OPT_REDUCE_TAIL)
 
 __all__ = [
     "load", "ImbdError", "MLP", "mlp_workspace_bytes", "mlp_workspace_offset", "mlp_fwd",

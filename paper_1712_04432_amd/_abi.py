@@ -12,8 +12,9 @@ IMBD_F32, IMBD_BF16 = 0, 1
 IMBD_WS_ACT, IMBD_WS_LOGITS, IMBD_WS_DY, IMBD_WS_ROWLOSS = 0, 1, 2, 3
 (IMBD_OPT_SKINNY_OFF, IMBD_OPT_SKINNY_SPLITS, IMBD_OPT_TOP_UNFUSED, IMBD_OPT_WIDE_OFF, IMBD_OPT_WIDE_SPLITS,
  IMBD_OPT_DW_WIDE_MIN_K, IMBD_OPT_DW_STREAM, IMBD_OPT_DW_GENERIC, IMBD_OPT_GEMM_CFG, IMBD_OPT_GEMM_SPLITS,
- IMBD_OPT_CONV_NT, IMBD_OPT_SKINNY_NB, IMBD_OPT_DW_WIDE_DUAL, IMBD_OPT_LOCAL_PAIR) = range(14)
-IMBD_OPT_COUNT = 14
+ IMBD_OPT_CONV_NT, IMBD_OPT_SKINNY_NB, IMBD_OPT_DW_WIDE_DUAL, IMBD_OPT_LOCAL_PAIR,
+ IMBD_OPT_REDUCE_TAIL) = range(15)
+IMBD_OPT_COUNT = 15
 IMBD_STATIC_SCRATCH_BYTES = 64 << 20
 (IMBD_K_GEMM_FWD, IMBD_K_GEMM_DX, IMBD_K_GEMM_DW, IMBD_K_SPLITK, IMBD_K_SOFTMAX, IMBD_K_BIAS,
  IMBD_K_SGD, IMBD_K_CAST, IMBD_K_CONV_FWD, IMBD_K_CONV_DGRAD, IMBD_K_CONV_WGRAD) = range(11)

@@ -329,6 +329,36 @@ static int bwd_impl(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, v
     imbd_layer &ly = layers[i - 1];
     const void *dy = at(ws, lay.dy[i]);
     const void *xi = (i == 1) ? x : at(ws, lay.act[i - 1]);
+    // Delta_W_i with the bias gradient from the same pass (row sums of the Delta_Y tile)
+    GemmProblem pw = dw_problem(d, i);
+    pw.A = xi;
+    pw.B = dy;
+    pw.db_mode = fuse_sgd ? 2 : 1;
+    pw.db_out = ly.db;
+    pw.bias = ly.b;
+    pw.bias_lr = lr;
+    {
+      Epilogue &e = pw.epi;
+      if (fuse_sgd) {
+        e.mode = EPI_SGD;
+        e.out = ly.w;
+        e.ldo = d->dims[i - 1];
+        e.out2 = (d->dtype == IMBD_BF16) ? reinterpret_cast<uint16_t *>(ly.w_lp) : nullptr;
+        e.ldo2 = d->dims[i - 1];
+        e.lr = lr;
+      } else {
+        e.mode = EPI_STORE;
+        e.out = ly.dw;
+        e.ldo = d->dims[i - 1];
+        e.out_dtype = IMBD_F32;
+      }
+    }
+    // The split-K reduce of Delta_X_i (into Delta_Y_{i-1}) rides on the update launch of
+    // layer i when that runs on the persistent kernel, whose MMA waves add the partials
+    // once their products are done: Delta_Y_{i-1} is first read by the next layer's
+    // launches, and the update kernel uses no workspace.
+    bool deferred = false;
+    SkReduceTail tail;
     if (i >= 2 || dx1) {
       GemmProblem p = dx_problem(d, i);
       p.A = ly.w_lp;
@@ -352,31 +382,11 @@ static int bwd_impl(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, v
         p.aux_scale = job->scale;
         job->pending = false;
       }
-      TRY(gemm_run(p, part, lay.partial_bytes, s));
+      if (i >= 2 && fuse_sgd && dw_sgd_route(pw)) TRY(gemm_run_defer(p, part, lay.partial_bytes, s, &deferred, &tail));
+      else TRY(gemm_run(p, part, lay.partial_bytes, s));
     }
-    // Delta_W_i with the bias gradient from the same pass (row sums of the Delta_Y tile)
-    GemmProblem p = dw_problem(d, i);
-    p.A = xi;
-    p.B = dy;
-    p.db_mode = fuse_sgd ? 2 : 1;
-    p.db_out = ly.db;
-    p.bias = ly.b;
-    p.bias_lr = lr;
-    Epilogue &e = p.epi;
-    if (fuse_sgd) {
-      e.mode = EPI_SGD;
-      e.out = ly.w;
-      e.ldo = d->dims[i - 1];
-      e.out2 = (d->dtype == IMBD_BF16) ? reinterpret_cast<uint16_t *>(ly.w_lp) : nullptr;
-      e.ldo2 = d->dims[i - 1];
-      e.lr = lr;
-    } else {
-      e.mode = EPI_STORE;
-      e.out = ly.dw;
-      e.ldo = d->dims[i - 1];
-      e.out_dtype = IMBD_F32;
-    }
-    TRY(gemm_run(p, part, lay.partial_bytes, s));
+    if (deferred) TRY(gemm_run_dw_tail(pw, part, lay.partial_bytes, s, tail));
+    else TRY(gemm_run(pw, part, lay.partial_bytes, s));
   }
   return IMBD_OK;
 }

@@ -116,6 +116,27 @@ bool skinny_dims_fit(const GemmProblem &p);  // the conditions on M, N, K, dtype
 bool skinny_fits(const GemmProblem &p);
 void skinny_plan(const GemmProblem &p, int *splits, int *k_split);
 int run_skinny(const GemmProblem &p, void *ws, hipStream_t s);
+// The skinny kernel's split-K reduce: its arguments, and the reduce left to a later launch.
+struct SkReduceArgs {
+  const float *partial;
+  int64_t tpitch, sstride;
+  int M, N, splits;
+  Epilogue epi;
+  const float *aux_rows;  // side job in one extra workgroup: *aux_loss = aux_scale * sum
+  float *aux_loss;
+  int aux_n;
+  float aux_scale;
+};
+struct SkReduceTail {
+  SkReduceArgs args;
+  int64_t items;  // one thread each (eight outputs of one sample), whole-vector accesses
+};
+// With deferred set, a reduce that one thread per item can do in its whole-vector form is
+// not launched but returned in *tail (*deferred = true): the caller hands it to a later
+// launch (run_dw_sgd) or to run_skinny_reduce_tail before anything reads the output or
+// overwrites the partials in ws.
+int run_skinny_split(const GemmProblem &p, void *ws, hipStream_t s, bool *deferred, SkReduceTail *tail);
+int run_skinny_reduce_tail(const SkReduceTail &tail, int layer, hipStream_t s);
 size_t skinny_ws_bytes(const GemmProblem &p);
 // Forward / Delta_X products for batches above 256 (bf16, B operand stored [n][k]):
 // whether the large-tile kernel takes the problem (its dimensions alone, or with the
@@ -143,7 +164,10 @@ int run_loss_mean(int B, const float *row_loss, float inv_batch, float *loss, hi
 // The persistent fused weight-gradient + update kernel (bf16, K <= 2048): whether it
 // takes the problem, and the launch.
 bool dw_sgd_fits(const GemmProblem &p);
-int run_dw_sgd(const GemmProblem &p, hipStream_t s);
+// tail: a skinny product's split-K reduce that the kernel's MMA waves run once their
+// products are done (while the update waves finish the last tile); the launch must not
+// write the reduce's partials or read its output.
+int run_dw_sgd(const GemmProblem &p, hipStream_t s, const SkReduceTail *tail = nullptr);
 // The weight gradient on large tiles (bf16; the SGD update past 256 samples or the fp32
 // store of alpha * Delta_W at any batch, in each tile's epilogue, the bias gradient on
 // the column-sum kernel): whether it takes the problem, and the launch.
@@ -151,6 +175,14 @@ bool dw_wide_fits(const GemmProblem &p);
 int run_dw_wide(const GemmProblem &p, hipStream_t s);
 // Enqueue the product; ws must hold plan.ws_bytes (partial sums) when splits > 1.
 int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s);
+// A Delta_X product whose split-K reduce a later launch may carry: as gemm_run, but on the
+// skinny kernel (option IMBD_OPT_REDUCE_TAIL on) a deferrable reduce comes back in *tail
+// (*deferred = true) instead of being launched; gemm_run_dw_tail then runs the weight
+// gradient with it (on the persistent update kernel, or after the reduce's own launch).
+bool dw_sgd_route(const GemmProblem &p);
+int gemm_run_defer(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, bool *deferred,
+                   SkReduceTail *tail);
+int gemm_run_dw_tail(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, const SkReduceTail &tail);
 
 // ----------------------------------------------------------------- other kernels
 // mean: also launch the batch mean of the per-sample losses into *loss (else the caller

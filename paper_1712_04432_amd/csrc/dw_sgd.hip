@@ -29,6 +29,7 @@
 #include <type_traits>
 
 #include "cdna4.h"
+#include "skinny_reduce.h"
 
 namespace imbd {
 namespace {
@@ -65,6 +66,8 @@ struct DwArgs {
   float db_alpha, bias_lr;
   int tiles_m, tiles_n;
   int spread;          // row-block order (see the kernel)
+  SkReduceArgs tail;   // a skinny product's split-K reduce carried by this launch
+  int64_t tail_items;  // its items (0: none)
 };
 
 // STREAM (batches past 256): Delta_Y travels in 32-sample slabs through a ring of its own,
@@ -334,6 +337,10 @@ __global__ void __launch_bounds__(512, 1) dw_sgd_kernel(DwArgs a) {
     }
     // Drain the ring's trailing loads (they target slots nobody reads again).
     asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
+    // The reduce this launch carries (another layer's Delta_X partials into its Delta_Y),
+    // spread over the workgroups' MMA waves while their update waves finish the last tile.
+    for (int64_t t = (int64_t)blockIdx.x * NTM + tid; t < a.tail_items; t += (int64_t)gridDim.x * NTM)
+      sk_reduce_item<true, 1>(a.tail, t);
   } else {
     // --------------------------------------------------------------- update group
     // Branch-free buffer loads and stores on per-tile descriptors. Rows past the matrix
@@ -450,8 +457,10 @@ bool dw_sgd_fits(const GemmProblem &p) {
          (int64_t)p.K * p.ldb * 2 < ((int64_t)1 << 31);
 }
 
-int run_dw_sgd(const GemmProblem &p, hipStream_t s) {
+int run_dw_sgd(const GemmProblem &p, hipStream_t s, const SkReduceTail *tail) {
   DwArgs d;
+  d.tail = tail ? tail->args : SkReduceArgs{};
+  d.tail_items = tail ? tail->items : 0;
   d.X = reinterpret_cast<const uint16_t *>(p.A);
   d.DY = reinterpret_cast<const uint16_t *>(p.B);
   d.ldx = p.lda;

@@ -973,6 +973,49 @@ int run_wide_softmax(const GemmProblem &p, void *ws, size_t ws_bytes, const int3
                                         dz_dtype, s);
 }
 
+// A fused-SGD weight-gradient problem that gemm_run sends to the persistent update kernel.
+bool dw_sgd_route(const GemmProblem &p) {
+  if (p.M <= 0 || p.N <= 0 || p.aux_loss || (p.db_mode != 0 && p.b_kc)) return false;
+  const GemmPlan pl = gemm_plan(p);
+  if (pl.cfg == PLAN_SKINNY || pl.cfg == PLAN_WIDE) return false;
+  return !dw_wide_fits(p) && dw_sgd_fits(p) && opt(IMBD_OPT_DW_GENERIC) == 0;
+}
+
+static int check_plan_ws(const GemmPlan &pl, const GemmProblem &p, const void *ws, size_t ws_bytes) {
+  if (pl.ws_bytes > 0 && (ws == nullptr || ws_bytes < pl.ws_bytes)) {
+    set_error("product %dx%dx%d needs %zu bytes of workspace for split-K partials, got %zu",
+              p.M, p.N, p.K, pl.ws_bytes, ws_bytes);
+    return IMBD_EWORKSPACE;
+  }
+  if (pl.ws_bytes > 0 && (uintptr_t)ws % 16 != 0) {
+    set_error("workspace must be 16-byte aligned");
+    return IMBD_EINVAL;
+  }
+  return IMBD_OK;
+}
+
+int gemm_run_defer(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, bool *deferred,
+                   SkReduceTail *tail) {
+  *deferred = false;
+  if (opt(IMBD_OPT_REDUCE_TAIL) != 0 && p.M > 0 && p.N > 0 && !p.aux_loss && !(p.db_mode != 0 && p.b_kc)) {
+    const GemmPlan pl = gemm_plan(p);
+    if (pl.cfg == PLAN_SKINNY) {
+      const int rc = check_plan_ws(pl, p, ws, ws_bytes);
+      if (rc != IMBD_OK) return rc;
+      return run_skinny_split(p, ws, s, deferred, tail);
+    }
+  }
+  return gemm_run(p, ws, ws_bytes, s);
+}
+
+int gemm_run_dw_tail(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, const SkReduceTail &tail) {
+  if (dw_sgd_route(p)) return run_dw_sgd(p, s, &tail);
+  // another route may use ws, where the partials are: the reduce goes first
+  const int rc = run_skinny_reduce_tail(tail, p.layer, s);
+  if (rc != IMBD_OK) return rc;
+  return gemm_run(p, ws, ws_bytes, s);
+}
+
 int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
   if (p.db_mode != 0 && p.b_kc) {
     set_error("bias sums need the B operand stored [k][n]");
@@ -989,14 +1032,9 @@ int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s) {
     return run_loss_mean(p.aux_n, p.aux_rows, p.aux_scale, p.aux_loss, s);
   }
   if (p.M <= 0 || p.N <= 0) return IMBD_OK;
-  if (pl.ws_bytes > 0 && (ws == nullptr || ws_bytes < pl.ws_bytes)) {
-    set_error("product %dx%dx%d needs %zu bytes of workspace for split-K partials, got %zu",
-              p.M, p.N, p.K, pl.ws_bytes, ws_bytes);
-    return IMBD_EWORKSPACE;
-  }
-  if (pl.ws_bytes > 0 && (uintptr_t)ws % 16 != 0) {
-    set_error("workspace must be 16-byte aligned");
-    return IMBD_EINVAL;
+  {
+    const int rc = check_plan_ws(pl, p, ws, ws_bytes);
+    if (rc != IMBD_OK) return rc;
   }
   if (pl.cfg == PLAN_SKINNY) return run_skinny(p, ws, s);
   const int esz = p.dtype == IMBD_BF16 ? 2 : 4;

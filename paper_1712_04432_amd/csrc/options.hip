@@ -36,6 +36,7 @@ const OptionDef kOptions[IMBD_OPT_COUNT] = {
     {"IMBD_SKINNY_NB", 0, 0, 4},         // skinny kernel's samples per workgroup / 64 (0: planner)
     {"IMBD_DW_WIDE_DUAL", -1, -1, 1},    // large-tile fused update, two workgroups per CU (-1: planner)
     {"IMBD_LOCAL_PAIR", 1, 0, 1},        // local backward: Delta_X and Delta_W products in one launch
+    {"IMBD_REDUCE_TAIL", 1, 0, 1},       // a Delta_X split reduce carried by the next update launch
 };
 
 std::atomic<int> g_opt[IMBD_OPT_COUNT];

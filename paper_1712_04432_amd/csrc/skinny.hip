@@ -26,6 +26,7 @@
 #include "dw_wide_body.h"
 #include "local_pair.h"
 #include "loss_mean.h"
+#include "skinny_reduce.h"
 
 namespace imbd {
 namespace {
@@ -414,26 +415,6 @@ __global__ void __launch_bounds__(512, 1) dx_dw_pair_kernel(SkArgs sk, DlArgs dl
   else if (bid >= n_pad) dw_wide_body<false, OH, false>(dl, smem, bid - n_pad, g_dl);
 }
 
-struct SkReduceArgs {
-  const float *partial;
-  int64_t tpitch, sstride;
-  int M, N, splits;
-  Epilogue epi;
-  const float *aux_rows;  // side job in one extra workgroup: *aux_loss = aux_scale * sum
-  float *aux_loss;
-  int aux_n;
-  float aux_scale;
-};
-
-// Adds the splits' partials and applies the store epilogue:
-// out(m, n) = [mask(m, n) > 0] * relu?(alpha * sum + bias[m]). Eight consecutive m of one
-// sample per group of LANES threads; VEC: every access is whole and aligned (checked on
-// the host). LANES = 1: one thread adds the splits in split order (the same order and
-// arithmetic as the split-K reduce of the tiled products). LANES = 4 (more than four
-// splits, where one thread would wait on its loads round after round): lane j adds splits
-// j, j+4, j+8, ... in that order, and the four sums are combined as (s0 + s1) + (s2 + s3)
-// by lane exchanges; each exchange adds the same two values on both lanes, so every lane
-// holds the same bits and the result is the same on every run.
 template <bool VEC, int LANES>
 __global__ void __launch_bounds__(256) skinny_reduce(SkReduceArgs g) {
   if (g.aux_loss && blockIdx.x == gridDim.x - 1) {
@@ -441,117 +422,7 @@ __global__ void __launch_bounds__(256) skinny_reduce(SkReduceArgs g) {
     block_loss_mean(g.aux_n, g.aux_rows, g.aux_scale, g.aux_loss, part);
     return;
   }
-  const int64_t tl = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t t = tl / LANES;
-  const int j = (int)(tl - t * LANES);
-  const int tile = (int)(t / ((int64_t)g.N * 8));
-  const int r = (int)(t - (int64_t)tile * g.N * 8);
-  const int n = r >> 3, m = tile * 64 + 8 * (r & 7);
-  if (n >= g.N || m >= g.M) return;  // the same for all LANES lanes of a group
-  const Epilogue &e = g.epi;
-  const float *p = g.partial + (int64_t)tile * g.tpitch + n * 64 + (m & 63);
-  f32x4 a0 = *reinterpret_cast<const f32x4 *>(p + (int64_t)j * g.sstride);
-  f32x4 a1 = *reinterpret_cast<const f32x4 *>(p + (int64_t)j * g.sstride + 4);
-  for (int s0 = j + LANES; s0 < g.splits; s0 += 4 * LANES) {
-    f32x4 q0[4], q1[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (s0 + u * LANES < g.splits) {
-        const float *q = p + (int64_t)(s0 + u * LANES) * g.sstride;
-        q0[u] = *reinterpret_cast<const f32x4 *>(q);
-        q1[u] = *reinterpret_cast<const f32x4 *>(q + 4);
-      }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (s0 + u * LANES < g.splits) {
-        a0 += q0[u];
-        a1 += q1[u];
-      }
-  }
-  if constexpr (LANES > 1) {
-#pragma unroll
-    for (int d = 1; d < LANES; d <<= 1)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        a0[i] += __shfl_xor(a0[i], d);
-        a1[i] += __shfl_xor(a1[i], d);
-      }
-    if (j != 0) return;
-  }
-  const float v[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
-  const int cnt = VEC ? 8 : min(8, g.M - m);
-  float x[8];
-  if constexpr (VEC) {
-    // bias, mask and output rows are whole and aligned (checked on the host)
-    float bb[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    if (e.bias) {
-      const f32x4 b0 = *reinterpret_cast<const f32x4 *>(e.bias + m);
-      const f32x4 b1 = *reinterpret_cast<const f32x4 *>(e.bias + m + 4);
-      bb[0] = b0[0]; bb[1] = b0[1]; bb[2] = b0[2]; bb[3] = b0[3];
-      bb[4] = b1[0]; bb[5] = b1[1]; bb[6] = b1[2]; bb[7] = b1[3];
-    }
-    bool keep[8] = {true, true, true, true, true, true, true, true};
-    if (e.mask) {
-      const int64_t off = (int64_t)n * e.ldmask + m;
-      if (e.mask_dtype == IMBD_BF16) {
-        const u32x4 mk = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint16_t *>(e.mask) + off);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) keep[i] = bf16_to_f32((uint16_t)((mk[i >> 1] >> (16 * (i & 1))) & 0xffffu)) > 0.0f;
-      } else {
-        const f32x4 m0 = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(e.mask) + off);
-        const f32x4 m1 = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(e.mask) + off + 4);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          keep[i] = m0[i] > 0.0f;
-          keep[i + 4] = m1[i] > 0.0f;
-        }
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      float y = e.alpha * v[i] + bb[i];
-      if (e.relu) y = y > 0.0f ? y : 0.0f;
-      x[i] = keep[i] ? y : 0.0f;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      if (i < cnt) {
-        float y = e.alpha * v[i] + (e.bias ? e.bias[m + i] : 0.0f);
-        if (e.relu) y = y > 0.0f ? y : 0.0f;
-        if (e.mask) {
-          const int64_t off = (int64_t)n * e.ldmask + m + i;
-          const float mk = e.mask_dtype == IMBD_BF16 ? bf16_to_f32(reinterpret_cast<const uint16_t *>(e.mask)[off])
-                                                     : reinterpret_cast<const float *>(e.mask)[off];
-          if (!(mk > 0.0f)) y = 0.0f;
-        }
-        x[i] = y;
-      }
-    }
-  }
-  if (e.out_dtype == IMBD_BF16) {
-    uint16_t *o = reinterpret_cast<uint16_t *>(e.out) + (int64_t)n * e.ldo + m;
-    if constexpr (VEC) {
-      u32x4 pk;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) pk[i] = (uint32_t)f32_to_bf16(x[2 * i]) | ((uint32_t)f32_to_bf16(x[2 * i + 1]) << 16);
-      *reinterpret_cast<u32x4 *>(o) = pk;
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        if (i < cnt) o[i] = f32_to_bf16(x[i]);
-    }
-  } else {
-    float *o = reinterpret_cast<float *>(e.out) + (int64_t)n * e.ldo + m;
-    if constexpr (VEC) {
-      *reinterpret_cast<f32x4 *>(o) = f32x4{x[0], x[1], x[2], x[3]};
-      *reinterpret_cast<f32x4 *>(o + 4) = f32x4{x[4], x[5], x[6], x[7]};
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        if (i < cnt) o[i] = x[i];
-    }
-  }
+  sk_reduce_item<VEC, LANES>(g, (int64_t)blockIdx.x * 256 + threadIdx.x);
 }
 
 struct SkSoftmaxArgs {
@@ -779,18 +650,16 @@ static int launch_skinny_product(const GemmProblem &p, void *ws, hipStream_t s, 
   return check_launch("skinny");
 }
 
-int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
-  SkArgs g;
-  int rc = launch_skinny_product(p, ws, s, &g, true);
-  if (rc != IMBD_OK || g.fused) return rc;
-  const int splits = g.splits;
+// The split-K reduce of a product whose partials launch_skinny_product left in ws.
+static SkReduceArgs skinny_reduce_args(const GemmProblem &p, const SkArgs &g, bool *vec, int *lanes,
+                                       int64_t *threads) {
   SkReduceArgs r;
   r.partial = g.partial;
   r.tpitch = g.tpitch;
   r.sstride = g.sstride;
   r.M = p.M;
   r.N = p.N;
-  r.splits = splits;
+  r.splits = g.splits;
   r.epi = p.epi;
   r.aux_rows = p.aux_rows;
   r.aux_loss = p.aux_n > 0 ? p.aux_loss : nullptr;
@@ -798,13 +667,18 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
   r.aux_scale = p.aux_scale;
   const Epilogue &e = p.epi;
   auto al = [](const void *q, int a) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % a) == 0; };
-  const bool vec = p.M % 8 == 0 && al(e.out, 16) && e.ldo % 8 == 0 && al(e.bias, 16) &&
-                   (e.mask == nullptr || (al(e.mask, 16) && e.ldmask % 8 == 0));
-  const int lanes = splits > 4 ? 4 : 1;
-  const int64_t threads = (int64_t)g.tiles_m * p.N * 8 * lanes;
+  *vec = p.M % 8 == 0 && al(e.out, 16) && e.ldo % 8 == 0 && al(e.bias, 16) &&
+         (e.mask == nullptr || (al(e.mask, 16) && e.ldmask % 8 == 0));
+  *lanes = g.splits > 4 ? 4 : 1;
+  *threads = (int64_t)g.tiles_m * p.N * 8 * *lanes;
+  return r;
+}
+
+static int launch_skinny_reduce(const SkReduceArgs &r, bool vec, int lanes, int64_t threads, int layer,
+                                hipStream_t s) {
   const unsigned blocks = (unsigned)((threads + 255) / 256) + (r.aux_loss ? 1u : 0u);
   {
-    LaunchTimer t(IMBD_K_SPLITK, p.layer, s);
+    LaunchTimer t(IMBD_K_SPLITK, layer, s);
     if (lanes == 4) {
       if (vec) hipLaunchKernelGGL((skinny_reduce<true, 4>), dim3(blocks), dim3(256), 0, s, r);
       else hipLaunchKernelGGL((skinny_reduce<false, 4>), dim3(blocks), dim3(256), 0, s, r);
@@ -814,6 +688,34 @@ int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
     }
   }
   return check_launch("skinny_reduce");
+}
+
+int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
+  SkReduceTail tail;
+  return run_skinny_split(p, ws, s, nullptr, &tail);
+}
+
+int run_skinny_split(const GemmProblem &p, void *ws, hipStream_t s, bool *deferred, SkReduceTail *tail) {
+  if (deferred) *deferred = false;
+  SkArgs g;
+  int rc = launch_skinny_product(p, ws, s, &g, true);
+  if (rc != IMBD_OK || g.fused) return rc;
+  bool vec;
+  int lanes;
+  int64_t threads;
+  const SkReduceArgs r = skinny_reduce_args(p, g, &vec, &lanes, &threads);
+  // a later launch may carry the reduce: one thread per item, the whole-vector form
+  if (deferred && vec && lanes == 1 && r.aux_loss == nullptr) {
+    tail->args = r;
+    tail->items = threads;
+    *deferred = true;
+    return IMBD_OK;
+  }
+  return launch_skinny_reduce(r, vec, lanes, threads, p.layer, s);
+}
+
+int run_skinny_reduce_tail(const SkReduceTail &tail, int layer, hipStream_t s) {
+  return launch_skinny_reduce(tail.args, true, 1, tail.items, layer, s);
 }
 
 bool skinny_softmax_fits(const GemmProblem &p) {

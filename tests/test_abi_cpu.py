@@ -156,7 +156,7 @@ class _Fake:
 
 _OPTION_DEFAULTS = {"SKINNY_OFF": 0, "SKINNY_SPLITS": 0, "TOP_UNFUSED": 0, "WIDE_OFF": 0, "WIDE_SPLITS": 0,
                     "DW_WIDE_MIN_K": 257, "DW_STREAM": 1, "DW_GENERIC": 0, "GEMM_CFG": -1, "GEMM_SPLITS": 0,
-                    "CONV_NT": 1, "SKINNY_NB": 0, "DW_WIDE_DUAL": -1, "LOCAL_PAIR": 1}
+                    "CONV_NT": 1, "SKINNY_NB": 0, "DW_WIDE_DUAL": -1, "LOCAL_PAIR": 1, "REDUCE_TAIL": 1}
 
 
 def _options_in_child(env_extra):

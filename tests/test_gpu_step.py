@@ -433,3 +433,33 @@ def test_wide_top_layer_softmax_one_pass_matches_two(imbd, dev):
     ref = oracle.train_step(d["w"], d["b"], xv, d["labels"], cfg.lr, "bf16")
     assert abs(out[0][1] - ref["loss"]) < TOL_BF16 * abs(ref["loss"])
     assert nrm_err(out[0][0], ref["logits"]) < TOL_BF16
+
+
+def test_dx_reduce_carried_by_update_launch_matches_own_launch(imbd, dev):
+    """At 256 samples the layer-2 Delta_X product's split-K partials are added (with the
+    ReLU mask, into Delta_Y_1) by the MMA waves of layer 2's update launch instead of a
+    reduce launch of its own (option reduce_tail). One full fused step of the
+    9216-4096-4096-1000 stack from the same seeded state both ways: one split reduce launch
+    fewer, and every output bit for bit the same (the same reduce arithmetic): fp32
+    masters, bf16 copies, biases, loss, hidden activations and every Delta_Y."""
+    import torch
+    cfg = get_config("alexnet_fc_b256")
+    _flush("Delta_X reduce carried by the update launch vs its own launch")
+    out = {}
+    for tail in (1, 0):
+        d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev, seed=6)
+        with imbd.options(reduce_tail=tail):
+            imbd.timing_begin(imbd.IMBD_K_SPLITK, -1, 64)
+            imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
+            n_red, _ = imbd.timing_end()
+        torch.cuda.synchronize()
+        out[tail] = {"n_red": n_red, "loss": loss.item(),
+                     "w": [host(l["w"]) for l in layers], "b": [host(l["b"]) for l in layers],
+                     "w16": [l["w_lp"].view(torch.int16).cpu().numpy() for l in layers],
+                     "act": [imbd.ws_view(net, ws, imbd.IMBD_WS_ACT, i).view(torch.int16).cpu().numpy() for i in (1, 2)],
+                     "dy": [imbd.ws_view(net, ws, imbd.IMBD_WS_DY, i).view(torch.int16).cpu().numpy() for i in (1, 2)]}
+    assert out[0]["n_red"] == out[1]["n_red"] + 1, (out[0]["n_red"], out[1]["n_red"])
+    assert out[0]["loss"] == out[1]["loss"]
+    for k in ("w", "b", "w16", "act", "dy"):
+        for i, (a, b) in enumerate(zip(out[0][k], out[1][k])):
+            assert np.array_equal(a, b), (k, i)
