@@ -354,11 +354,12 @@ static int bwd_impl(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, v
       }
     }
     // The split-K reduce of Delta_X_i (into Delta_Y_{i-1}) rides on the update launch of
-    // layer i when that runs on the persistent kernel, whose MMA waves add the partials
-    // once their products are done: Delta_Y_{i-1} is first read by the next layer's
-    // launches, and the update kernel uses no workspace.
+    // layer i when that runs on the persistent kernel (whose MMA waves add the partials
+    // once their products are done) or on the large-tile one (whose workgroups share the
+    // reduce out after their tiles): Delta_Y_{i-1} is first read by the next layer's
+    // launches, and neither update kernel uses the workspace.
     bool deferred = false;
-    SkReduceTail tail;
+    ReduceTail tail;
     if (i >= 2 || dx1) {
       GemmProblem p = dx_problem(d, i);
       p.A = ly.w_lp;
@@ -382,7 +383,8 @@ static int bwd_impl(const imbd_mlp_desc *d, imbd_layer *layers, const void *x, v
         p.aux_scale = job->scale;
         job->pending = false;
       }
-      if (i >= 2 && fuse_sgd && dw_sgd_route(pw)) TRY(gemm_run_defer(p, part, lay.partial_bytes, s, &deferred, &tail));
+      if (i >= 2 && fuse_sgd && (dw_sgd_route(pw) || dw_wide_route(pw)))
+        TRY(gemm_run_defer(p, part, lay.partial_bytes, s, &deferred, &tail));
       else TRY(gemm_run(p, part, lay.partial_bytes, s));
     }
     if (deferred) TRY(gemm_run_dw_tail(pw, part, lay.partial_bytes, s, tail));

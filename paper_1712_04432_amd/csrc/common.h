@@ -127,16 +127,29 @@ struct SkReduceArgs {
   int aux_n;
   float aux_scale;
 };
-struct SkReduceTail {
-  SkReduceArgs args;
-  int64_t items;  // one thread each (eight outputs of one sample), whole-vector accesses
+// The lean split-K reduce of the wide-batch and tiled products (partials [split][n][ldp]).
+struct LeanReduceArgs {
+  const float *partial;
+  int64_t ldp, sstride;
+  int M, N, splits;
+  Epilogue epi;
+};
+// A split-K reduce left to a later launch: kind 1 the skinny kernel's (sk), kind 2 the lean
+// one with the mask and a bf16 output (lean); items: one thread each (eight outputs of one
+// sample), whole-vector accesses.
+struct ReduceTail {
+  int kind = 0;
+  SkReduceArgs sk;
+  LeanReduceArgs lean;
+  int64_t items = 0;
 };
 // With deferred set, a reduce that one thread per item can do in its whole-vector form is
 // not launched but returned in *tail (*deferred = true): the caller hands it to a later
-// launch (run_dw_sgd) or to run_skinny_reduce_tail before anything reads the output or
-// overwrites the partials in ws.
-int run_skinny_split(const GemmProblem &p, void *ws, hipStream_t s, bool *deferred, SkReduceTail *tail);
-int run_skinny_reduce_tail(const SkReduceTail &tail, int layer, hipStream_t s);
+// launch (run_dw_sgd) or to run_reduce_tail before anything reads the output or overwrites
+// the partials in ws.
+int run_skinny_split(const GemmProblem &p, void *ws, hipStream_t s, bool *deferred, ReduceTail *tail);
+int run_reduce_tail(const ReduceTail &tail, int layer, hipStream_t s);  // the reduce's own launch
+int run_skinny_reduce_tail(const ReduceTail &tail, int layer, hipStream_t s);  // ... of kind 1
 size_t skinny_ws_bytes(const GemmProblem &p);
 // Forward / Delta_X products for batches above 256 (bf16, B operand stored [n][k]):
 // whether the large-tile kernel takes the problem (its dimensions alone, or with the
@@ -167,22 +180,28 @@ bool dw_sgd_fits(const GemmProblem &p);
 // tail: a skinny product's split-K reduce that the kernel's MMA waves run once their
 // products are done (while the update waves finish the last tile); the launch must not
 // write the reduce's partials or read its output.
-int run_dw_sgd(const GemmProblem &p, hipStream_t s, const SkReduceTail *tail = nullptr);
+int run_dw_sgd(const GemmProblem &p, hipStream_t s, const ReduceTail *tail = nullptr);
 // The weight gradient on large tiles (bf16; the SGD update past 256 samples or the fp32
 // store of alpha * Delta_W at any batch, in each tile's epilogue, the bias gradient on
 // the column-sum kernel): whether it takes the problem, and the launch.
 bool dw_wide_fits(const GemmProblem &p);
-int run_dw_wide(const GemmProblem &p, hipStream_t s);
+// tail (kind 2, fused update only): a wide-batch product's split-K reduce that every
+// workgroup takes a share of after its tile; the launch must not write the reduce's
+// partials or read its output.
+int run_dw_wide(const GemmProblem &p, hipStream_t s, const ReduceTail *tail = nullptr);
 // Enqueue the product; ws must hold plan.ws_bytes (partial sums) when splits > 1.
 int gemm_run(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s);
 // A Delta_X product whose split-K reduce a later launch may carry: as gemm_run, but on the
-// skinny kernel (option IMBD_OPT_REDUCE_TAIL on) a deferrable reduce comes back in *tail
-// (*deferred = true) instead of being launched; gemm_run_dw_tail then runs the weight
-// gradient with it (on the persistent update kernel, or after the reduce's own launch).
+// skinny or wide-batch kernel (option IMBD_OPT_REDUCE_TAIL on) a deferrable reduce comes
+// back in *tail (*deferred = true) instead of being launched; gemm_run_dw_tail then runs the
+// weight gradient with it (on the update kernel that can carry it, or after the reduce's own
+// launch). dw_sgd_route / dw_wide_route: the fused update problems that gemm_run sends to
+// the persistent kernel / the large-tile kernel.
 bool dw_sgd_route(const GemmProblem &p);
+bool dw_wide_route(const GemmProblem &p);
 int gemm_run_defer(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, bool *deferred,
-                   SkReduceTail *tail);
-int gemm_run_dw_tail(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, const SkReduceTail &tail);
+                   ReduceTail *tail);
+int gemm_run_dw_tail(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, const ReduceTail &tail);
 
 // ----------------------------------------------------------------- other kernels
 // mean: also launch the batch mean of the per-sample losses into *loss (else the caller

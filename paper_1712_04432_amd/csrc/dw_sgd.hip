@@ -457,10 +457,11 @@ bool dw_sgd_fits(const GemmProblem &p) {
          (int64_t)p.K * p.ldb * 2 < ((int64_t)1 << 31);
 }
 
-int run_dw_sgd(const GemmProblem &p, hipStream_t s, const SkReduceTail *tail) {
+int run_dw_sgd(const GemmProblem &p, hipStream_t s, const ReduceTail *tail) {
   DwArgs d;
-  d.tail = tail ? tail->args : SkReduceArgs{};
-  d.tail_items = tail ? tail->items : 0;
+  const bool carry = tail && tail->kind == 1;
+  d.tail = carry ? tail->sk : SkReduceArgs{};
+  d.tail_items = carry ? tail->items : 0;
   d.X = reinterpret_cast<const uint16_t *>(p.A);
   d.DY = reinterpret_cast<const uint16_t *>(p.B);
   d.ldx = p.lda;

@@ -28,6 +28,7 @@
 #include <stdlib.h>
 
 #include "dw_wide_body.h"
+#include "lean_reduce.h"
 
 namespace imbd {
 namespace {
@@ -37,6 +38,15 @@ template <bool SGD, int OH, bool DUAL>
 __global__ void __launch_bounds__(512, DUAL ? 2 : 1) dw_wide_kernel(DlArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[dl_lds_bytes<OH, DUAL>()];
   dw_wide_body<SGD, OH, DUAL>(a, smem, (int)blockIdx.x, (int)gridDim.x);
+  if constexpr (SGD) {
+    // the reduce this launch carries (another layer's Delta_X partials into its Delta_Y):
+    // eight outputs of one sample per item, a share of them per workgroup after its tile
+    const int mq = a.tail.M / 8;
+    for (int64_t t = (int64_t)blockIdx.x * 512 + threadIdx.x; t < a.tail_items; t += (int64_t)gridDim.x * 512) {
+      const int n = (int)(t / mq);
+      lean_reduce_item<true, true>(a.tail, n, (int)(t - (int64_t)n * mq) * 8);
+    }
+  }
 }
 
 }  // namespace
@@ -115,18 +125,27 @@ void dw_wide_prepare(const GemmProblem &p, int extra_blocks, DlArgs *out, int *o
   a.bias_lr = p.bias_lr;
   a.db_out = p.db_out;
   a.bias = p.bias;
+  a.tail = LeanReduceArgs{};
+  a.tail_items = 0;
   *out = a;
   *oh_out = oh;
   *dual_out = dual;
   *grid_out = (a.tiles_o * a.tiles_i + 7) / 8 * 8;
 }
 
-int run_dw_wide(const GemmProblem &p, hipStream_t s) {
+int run_dw_wide(const GemmProblem &p, hipStream_t s, const ReduceTail *tail) {
   DlArgs a;
   int oh, grid;
   bool dual;
   dw_wide_prepare(p, 0, &a, &oh, &dual, &grid);
   const bool sgd = p.epi.mode == EPI_SGD, half = oh == 128;
+  if (tail && tail->kind == 2 && sgd) {
+    a.tail = tail->lean;
+    a.tail_items = tail->items;
+  } else if (tail && tail->kind != 0) {
+    set_error("the large-tile update carries only a wide-batch product's reduce");
+    return IMBD_EINVAL;
+  }
   {
     LaunchTimer t(p.kclass, p.layer, s);
     if (dual) {

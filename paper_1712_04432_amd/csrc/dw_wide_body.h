@@ -36,6 +36,10 @@ struct DlArgs {
   float *db_out, *bias;
   // Delta_Y's rows only 4-byte aligned (pitch and base): loaded in 4-byte pieces
   int dy_dw4;
+  // a wide-batch product's split-K reduce (mask, bf16 output) carried by the fused-update
+  // launch: its tail_items items shared out over the workgroups after their tiles
+  LeanReduceArgs tail;
+  int64_t tail_items;
 };
 
 __device__ __forceinline__ int dl_swz(int r) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1); }

@@ -29,6 +29,7 @@
 #include <algorithm>
 
 #include "common.h"
+#include "lean_reduce.h"
 
 namespace imbd {
 
@@ -726,71 +727,7 @@ __global__ void __launch_bounds__(256) splitk_reduce_fast(KArgs g) {
   const int n = blockIdx.y;
   const int m = (blockIdx.x * 256 + threadIdx.x) * 8;
   if (m >= g.M) return;
-  const Epilogue &e = g.epi;
-  const float *p0 = g.partial + (int64_t)n * g.ldp + m;
-  f32x4 a0 = *reinterpret_cast<const f32x4 *>(p0);
-  f32x4 a1 = *reinterpret_cast<const f32x4 *>(p0 + 4);
-  for (int s0 = 1; s0 < g.splits; s0 += 4) {
-    f32x4 q0[4], q1[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (s0 + u < g.splits) {
-        const float *p = p0 + (int64_t)(s0 + u) * g.sstride;
-        q0[u] = *reinterpret_cast<const f32x4 *>(p);
-        q1[u] = *reinterpret_cast<const f32x4 *>(p + 4);
-      }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (s0 + u < g.splits) {
-        a0 += q0[u];
-        a1 += q1[u];
-      }
-  }
-  float x[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
-  if (e.bias) {
-    const f32x4 b0 = *reinterpret_cast<const f32x4 *>(e.bias + m);
-    const f32x4 b1 = *reinterpret_cast<const f32x4 *>(e.bias + m + 4);
-    const float bb[8] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = e.alpha * x[i] + bb[i];
-  } else {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = e.alpha * x[i];
-  }
-  if (e.relu) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = x[i] > 0.f ? x[i] : 0.f;
-  }
-  if constexpr (MASK) {
-    // mask element type follows the activation type (bf16 here, fp32 for fp32 networks)
-    const int64_t off = (int64_t)n * e.ldmask + m;
-    if (e.mask_dtype == IMBD_BF16) {
-      const u32x4 mk = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint16_t *>(e.mask) + off);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const uint16_t h = (uint16_t)((mk[i >> 1] >> (16 * (i & 1))) & 0xffffu);
-        if (!(bf16_to_f32(h) > 0.f)) x[i] = 0.f;
-      }
-    } else {
-      const f32x4 m0 = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(e.mask) + off);
-      const f32x4 m1 = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(e.mask) + off + 4);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (!(m0[i] > 0.f)) x[i] = 0.f;
-        if (!(m1[i] > 0.f)) x[i + 4] = 0.f;
-      }
-    }
-  }
-  if constexpr (OUT_BF16) {
-    u32x4 pk;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pk[i] = pack_bf16x2(x[2 * i], x[2 * i + 1]);
-    *reinterpret_cast<u32x4 *>(reinterpret_cast<uint16_t *>(e.out) + (int64_t)n * e.ldo + m) = pk;
-  } else {
-    float *o = reinterpret_cast<float *>(e.out) + (int64_t)n * e.ldo + m;
-    *reinterpret_cast<f32x4 *>(o) = f32x4{x[0], x[1], x[2], x[3]};
-    *reinterpret_cast<f32x4 *>(o + 4) = f32x4{x[4], x[5], x[6], x[7]};
-  }
+  lean_reduce_item<OUT_BF16, MASK>(LeanReduceArgs{g.partial, g.ldp, g.sstride, g.M, g.N, g.splits, g.epi}, n, m);
 }
 
 // ------------------------------------------------------------- configurations
@@ -919,14 +856,19 @@ GemmPlan gemm_plan(const GemmProblem &p) {
 }
 
 // Adds the split partials in split order and applies the epilogue.
-static int launch_reduce(const GemmProblem &p, const KArgs &g, hipStream_t s) {
-  // the lean kernel needs 8-aligned rows (M, ld and pointers) and a store epilogue
+// the lean reduce needs 8-aligned rows (M, ld and pointers) and a store epilogue
+static bool lean_ok(const GemmProblem &p, int64_t ldp, int64_t sstride) {
   const Epilogue &e = p.epi;
   const int oes = e.out_dtype == IMBD_BF16 ? 2 : 4;
-  const bool lean = e.mode == EPI_STORE && p.M % 8 == 0 && e.ldo % 8 == 0 && (uintptr_t)e.out % (8 * oes) == 0 &&
-                    (!e.bias || (uintptr_t)e.bias % 32 == 0) &&
-                    (!e.mask || (e.ldmask % 8 == 0 && (uintptr_t)e.mask % (e.mask_dtype == IMBD_BF16 ? 16 : 32) == 0)) &&
-                    g.ldp % 8 == 0 && g.sstride % 8 == 0 && p.N <= 65535;
+  return e.mode == EPI_STORE && p.M % 8 == 0 && e.ldo % 8 == 0 && (uintptr_t)e.out % (8 * oes) == 0 &&
+         (!e.bias || (uintptr_t)e.bias % 32 == 0) &&
+         (!e.mask || (e.ldmask % 8 == 0 && (uintptr_t)e.mask % (e.mask_dtype == IMBD_BF16 ? 16 : 32) == 0)) &&
+         ldp % 8 == 0 && sstride % 8 == 0 && p.N <= 65535;
+}
+
+static int launch_reduce(const GemmProblem &p, const KArgs &g, hipStream_t s) {
+  const Epilogue &e = p.epi;
+  const bool lean = lean_ok(p, g.ldp, g.sstride);
   LaunchTimer t(IMBD_K_SPLITK, p.layer, s);
   if (lean) {
     const dim3 grid((unsigned)((p.M / 8 + 255) / 256), (unsigned)p.N);
@@ -981,6 +923,13 @@ bool dw_sgd_route(const GemmProblem &p) {
   return !dw_wide_fits(p) && dw_sgd_fits(p) && opt(IMBD_OPT_DW_GENERIC) == 0;
 }
 
+bool dw_wide_route(const GemmProblem &p) {
+  if (p.M <= 0 || p.N <= 0 || p.aux_loss || (p.db_mode != 0 && p.b_kc) || p.epi.mode != EPI_SGD) return false;
+  const GemmPlan pl = gemm_plan(p);
+  if (pl.cfg == PLAN_SKINNY || pl.cfg == PLAN_WIDE) return false;
+  return dw_wide_fits(p);
+}
+
 static int check_plan_ws(const GemmPlan &pl, const GemmProblem &p, const void *ws, size_t ws_bytes) {
   if (pl.ws_bytes > 0 && (ws == nullptr || ws_bytes < pl.ws_bytes)) {
     set_error("product %dx%dx%d needs %zu bytes of workspace for split-K partials, got %zu",
@@ -995,23 +944,59 @@ static int check_plan_ws(const GemmPlan &pl, const GemmProblem &p, const void *w
 }
 
 int gemm_run_defer(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, bool *deferred,
-                   SkReduceTail *tail) {
+                   ReduceTail *tail) {
   *deferred = false;
-  if (opt(IMBD_OPT_REDUCE_TAIL) != 0 && p.M > 0 && p.N > 0 && !p.aux_loss && !(p.db_mode != 0 && p.b_kc)) {
+  // (a loss-mean side job stays where gemm_run puts it: in the wide-batch product launch,
+  // or in the skinny reduce, which is then not deferred)
+  if (opt(IMBD_OPT_REDUCE_TAIL) != 0 && p.M > 0 && p.N > 0 && !(p.db_mode != 0 && p.b_kc)) {
     const GemmPlan pl = gemm_plan(p);
     if (pl.cfg == PLAN_SKINNY) {
       const int rc = check_plan_ws(pl, p, ws, ws_bytes);
       if (rc != IMBD_OK) return rc;
       return run_skinny_split(p, ws, s, deferred, tail);
     }
+    const Epilogue &e = p.epi;
+    if (pl.cfg == PLAN_WIDE && pl.splits > 1 && e.mask && e.mask_dtype == IMBD_BF16 && e.out_dtype == IMBD_BF16) {
+      int rc = check_plan_ws(pl, p, ws, ws_bytes);
+      if (rc != IMBD_OK) return rc;
+      LeanReduceArgs r{reinterpret_cast<float *>(ws), partial_ld(p.M), partial_split_stride(p.M, p.N), p.M, p.N,
+                       pl.splits, e};
+      if (lean_ok(p, r.ldp, r.sstride)) {
+        rc = run_wide(p, reinterpret_cast<float *>(ws), r.ldp, r.sstride, s);
+        if (rc != IMBD_OK) return rc;
+        tail->kind = 2;
+        tail->lean = r;
+        tail->items = (int64_t)p.N * (p.M / 8);
+        *deferred = true;
+        return IMBD_OK;
+      }
+    }
   }
   return gemm_run(p, ws, ws_bytes, s);
 }
 
-int gemm_run_dw_tail(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, const SkReduceTail &tail) {
-  if (dw_sgd_route(p)) return run_dw_sgd(p, s, &tail);
+int run_reduce_tail(const ReduceTail &tail, int layer, hipStream_t s) {
+  if (tail.kind == 1) return run_skinny_reduce_tail(tail, layer, s);
+  if (tail.kind != 2) return IMBD_OK;
+  KArgs g{};
+  g.M = tail.lean.M;
+  g.N = tail.lean.N;
+  g.splits = tail.lean.splits;
+  g.epi = tail.lean.epi;
+  g.partial = const_cast<float *>(tail.lean.partial);
+  g.ldp = tail.lean.ldp;
+  g.sstride = tail.lean.sstride;
+  LaunchTimer t(IMBD_K_SPLITK, layer, s);
+  const dim3 grid((unsigned)((g.M / 8 + 255) / 256), (unsigned)g.N);
+  hipLaunchKernelGGL((splitk_reduce_fast<true, true>), grid, dim3(256), 0, s, g);
+  return check_launch("splitk_reduce");
+}
+
+int gemm_run_dw_tail(const GemmProblem &p, void *ws, size_t ws_bytes, hipStream_t s, const ReduceTail &tail) {
+  if (tail.kind == 1 && dw_sgd_route(p)) return run_dw_sgd(p, s, &tail);
+  if (tail.kind == 2 && dw_wide_route(p)) return run_dw_wide(p, s, &tail);
   // another route may use ws, where the partials are: the reduce goes first
-  const int rc = run_skinny_reduce_tail(tail, p.layer, s);
+  const int rc = run_reduce_tail(tail, p.layer, s);
   if (rc != IMBD_OK) return rc;
   return gemm_run(p, ws, ws_bytes, s);
 }

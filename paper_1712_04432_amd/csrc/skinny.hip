@@ -691,11 +691,11 @@ static int launch_skinny_reduce(const SkReduceArgs &r, bool vec, int lanes, int6
 }
 
 int run_skinny(const GemmProblem &p, void *ws, hipStream_t s) {
-  SkReduceTail tail;
+  ReduceTail tail;
   return run_skinny_split(p, ws, s, nullptr, &tail);
 }
 
-int run_skinny_split(const GemmProblem &p, void *ws, hipStream_t s, bool *deferred, SkReduceTail *tail) {
+int run_skinny_split(const GemmProblem &p, void *ws, hipStream_t s, bool *deferred, ReduceTail *tail) {
   if (deferred) *deferred = false;
   SkArgs g;
   int rc = launch_skinny_product(p, ws, s, &g, true);
@@ -706,7 +706,8 @@ int run_skinny_split(const GemmProblem &p, void *ws, hipStream_t s, bool *deferr
   const SkReduceArgs r = skinny_reduce_args(p, g, &vec, &lanes, &threads);
   // a later launch may carry the reduce: one thread per item, the whole-vector form
   if (deferred && vec && lanes == 1 && r.aux_loss == nullptr) {
-    tail->args = r;
+    tail->kind = 1;
+    tail->sk = r;
     tail->items = threads;
     *deferred = true;
     return IMBD_OK;
@@ -714,8 +715,8 @@ int run_skinny_split(const GemmProblem &p, void *ws, hipStream_t s, bool *deferr
   return launch_skinny_reduce(r, vec, lanes, threads, p.layer, s);
 }
 
-int run_skinny_reduce_tail(const SkReduceTail &tail, int layer, hipStream_t s) {
-  return launch_skinny_reduce(tail.args, true, 1, tail.items, layer, s);
+int run_skinny_reduce_tail(const ReduceTail &tail, int layer, hipStream_t s) {
+  return launch_skinny_reduce(tail.sk, true, 1, tail.items, layer, s);
 }
 
 bool skinny_softmax_fits(const GemmProblem &p) {

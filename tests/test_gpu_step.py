@@ -463,3 +463,33 @@ def test_dx_reduce_carried_by_update_launch_matches_own_launch(imbd, dev):
     for k in ("w", "b", "w16", "act", "dy"):
         for i, (a, b) in enumerate(zip(out[0][k], out[1][k])):
             assert np.array_equal(a, b), (k, i)
+
+
+def test_wide_dx_reduce_carried_by_update_launch_matches_own_launch(imbd, dev):
+    """Past 256 samples a layer's Delta_X split-K partials are added (with the ReLU mask,
+    into the Delta_Y of the layer below) by the workgroups of that layer's large-tile update
+    launch after their tiles, instead of a reduce launch of its own (option reduce_tail). A
+    2048-2048-2048-1000 stack at 512 samples, the wide-batch products split in K two ways:
+    two split reduce launches fewer (layers 3 and 2), and every output bit for bit the
+    same: fp32 masters, bf16 copies, biases, loss, hidden activations and every Delta_Y."""
+    import torch
+    cfg = scaled_mlp((2048, 2048, 2048, 1000), 512, "bf16")
+    _flush("wide Delta_X reduce carried by the update launch vs its own launch")
+    out = {}
+    for tail in (1, 0):
+        d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev, seed=8)
+        with imbd.options(reduce_tail=tail, wide_splits=2):
+            imbd.timing_begin(imbd.IMBD_K_SPLITK, -1, 64)
+            imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
+            n_red, _ = imbd.timing_end()
+        torch.cuda.synchronize()
+        out[tail] = {"n_red": n_red, "loss": loss.item(),
+                     "w": [host(l["w"]) for l in layers], "b": [host(l["b"]) for l in layers],
+                     "w16": [l["w_lp"].view(torch.int16).cpu().numpy() for l in layers],
+                     "act": [imbd.ws_view(net, ws, imbd.IMBD_WS_ACT, i).view(torch.int16).cpu().numpy() for i in (1, 2)],
+                     "dy": [imbd.ws_view(net, ws, imbd.IMBD_WS_DY, i).view(torch.int16).cpu().numpy() for i in (1, 2, 3)]}
+    assert out[0]["n_red"] == out[1]["n_red"] + 2, (out[0]["n_red"], out[1]["n_red"])
+    assert out[0]["loss"] == out[1]["loss"]
+    for k in ("w", "b", "w16", "act", "dy"):
+        for i, (a, b) in enumerate(zip(out[0][k], out[1][k])):
+            assert np.array_equal(a, b), (k, i)
