@@ -266,8 +266,8 @@ enum imbd_option {
                                    (128-row tiles): 1 always, 0 never, -1 = planned (-1..1) */
     IMBD_OPT_LOCAL_PAIR = 13,   /* 0: the local backward pass's Delta_X and Delta_W products in two
                                    launches instead of one (default 1) */
-    IMBD_OPT_REDUCE_TAIL = 14,  /* 0: a layer's Delta_X split-K reduce (B <= 256) in a launch of its
-                                   own instead of carried by that layer's update launch (default 1) */
+    IMBD_OPT_REDUCE_TAIL = 14,  /* 0: a layer's Delta_X split-K reduce in a launch of its own instead
+                                   of carried by that layer's update launch (default 1) */
     IMBD_OPT_COUNT = 15
 };
 /* Each option starts at the value of the environment variable named by
