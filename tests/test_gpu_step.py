@@ -465,20 +465,25 @@ def test_dx_reduce_carried_by_update_launch_matches_own_launch(imbd, dev):
             assert np.array_equal(a, b), (k, i)
 
 
-def test_wide_dx_reduce_carried_by_update_launch_matches_own_launch(imbd, dev):
+@pytest.mark.parametrize("update", ["large_tile", "persistent"])
+def test_wide_dx_reduce_carried_by_update_launch_matches_own_launch(imbd, dev, update):
     """Past 256 samples a layer's Delta_X split-K partials are added (with the ReLU mask,
     into the Delta_Y of the layer below) by the workgroups of that layer's large-tile update
     launch after their tiles, instead of a reduce launch of its own (option reduce_tail). A
     2048-2048-2048-1000 stack at 512 samples, the wide-batch products split in K two ways:
     two split reduce launches fewer (layers 3 and 2), and every output bit for bit the
-    same: fp32 masters, bf16 copies, biases, loss, hidden activations and every Delta_Y."""
+    same: fp32 masters, bf16 copies, biases, loss, hidden activations and every Delta_Y.
+    With the update forced onto the persistent kernel (which carries only the skinny
+    kernel's reduce) the deferred reduce gets its own launch before the update: the same
+    launch count and bits."""
     import torch
     cfg = scaled_mlp((2048, 2048, 2048, 1000), 512, "bf16")
-    _flush("wide Delta_X reduce carried by the update launch vs its own launch")
+    _flush(f"wide Delta_X reduce carried by the update launch vs its own launch ({update} update)")
+    route = {} if update == "large_tile" else {"dw_wide_min_k": 100000}
     out = {}
     for tail in (1, 0):
         d, net, layers, x, xv, lab, ws, loss = _setup(imbd, cfg, dev, seed=8)
-        with imbd.options(reduce_tail=tail, wide_splits=2):
+        with imbd.options(reduce_tail=tail, wide_splits=2, **route):
             imbd.timing_begin(imbd.IMBD_K_SPLITK, -1, 64)
             imbd.mlp_train_step(net, layers, x, lab, ws, cfg.lr, loss)
             n_red, _ = imbd.timing_end()
@@ -488,7 +493,8 @@ def test_wide_dx_reduce_carried_by_update_launch_matches_own_launch(imbd, dev):
                      "w16": [l["w_lp"].view(torch.int16).cpu().numpy() for l in layers],
                      "act": [imbd.ws_view(net, ws, imbd.IMBD_WS_ACT, i).view(torch.int16).cpu().numpy() for i in (1, 2)],
                      "dy": [imbd.ws_view(net, ws, imbd.IMBD_WS_DY, i).view(torch.int16).cpu().numpy() for i in (1, 2, 3)]}
-    assert out[0]["n_red"] == out[1]["n_red"] + 2, (out[0]["n_red"], out[1]["n_red"])
+    carried = 2 if update == "large_tile" else 0
+    assert out[0]["n_red"] == out[1]["n_red"] + carried, (out[0]["n_red"], out[1]["n_red"])
     assert out[0]["loss"] == out[1]["loss"]
     for k in ("w", "b", "w16", "act", "dy"):
         for i, (a, b) in enumerate(zip(out[0][k], out[1][k])):
